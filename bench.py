@@ -1,0 +1,219 @@
+#!/usr/bin/env python3
+"""Benchmark of the decode / verify attention hot path on one MI355X.
+
+One step = one ts_decode_attn call (plan + launch, split-KV streaming
+kernel, log-sum-exp merge) over one batch of the bulk-pool workload: 256
+sequences, one query token each, 32 query / 8 KV heads, head_dim 128,
+context = prompt U{256..1024} + response min(lognormal(median 2048,
+sigma 0.8), 16384), page size 16, bf16 N(0,1) values, seed 0.  Inputs are
+resident in HBM before timing; calls rotate over distinct KV pools (like the
+layers of a model) so the 256 MB last-level cache cannot serve a pool twice
+in a row.
+
+Printed: one JSON line with the bulk KV GB/s as ``value``, the roofline of
+the streaming kernel (its average duration from HIP events recorded around
+it on its own stream), the float64 oracle timed on this host's cores, the
+two tail-pool verify workloads and the concurrency curve (seed 0).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_GBPS = 8000.0          # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = ["attn_common.h", "attn_decode.hip", "attn_verify.hip", "attn_merge.hip", "api.hip"]
+
+WORKLOADS = {
+    "bulk": "bulk pool decode: 256 seqs, q_len 1, 32 q / 8 kv heads, d128, page 16, "
+            "ctx = U{256..1024} + min(lognormal(median 2048, sigma 0.8), 16384), bf16 N(0,1), seed 0",
+    "mtp": "tail pool MTP verify: 8 seqs, q_len 4 causal, 32/8 heads, d128, ctx U{16384..65536}",
+    "dflash": "tail pool block-draft verify: 4 seqs, q_len 16 causal, 32/8 heads, d128, "
+              "ctx U{32768..98304}",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_22788_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(name: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they
+    were taken on the current kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    rec = data.get(name)
+    if not rec or rec.get("kernel_hash") != kernel_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def make_pools(wl, n_pools):
+    """n_pools copies of the KV pool: pool 0 holds the workload's values,
+    pool p the next values of the same streams."""
+    import torch
+    from paper_2608_22788_amd import binding, device, synth
+    t = device.upload(wl, values="device")
+    pools = [(t["k_pages"], t["v_pages"])]
+    elems = t["k_pages"].numel()
+    for p in range(1, n_pools):
+        k = torch.empty_like(t["k_pages"])
+        v = torch.empty_like(t["v_pages"])
+        binding.synth_fill(k, wl.seed, synth.S_K, p * elems)
+        binding.synth_fill(v, wl.seed, synth.S_V, p * elems)
+        pools.append((k, v))
+    return t, pools
+
+
+def time_workload(name, steps, warmup, min_rotation=4 << 30):
+    import torch
+    from paper_2608_22788_amd import binding, synth
+    wl = synth.make_workload(name, seed=0)
+    kv = wl.kv_bytes()
+    n_pools = max(2, -(-min_rotation // kv))
+    log(f"[bench] {name}: B={wl.B} q_len={wl.Qmax} sum_ctx={int(wl.ctx_lens.sum())} "
+        f"KV={kv / 1e9:.3f} GB pools={n_pools}")
+    t, pools = make_pools(wl, n_pools)
+    shape = binding.shape_of(t["q"], t["k_pages"], t["page_table"], wl.max_ctx_len)
+    ws = torch.empty(binding.workspace_size(shape), dtype=torch.uint8, device="cuda")
+    ev = [(binding.Event(), binding.Event()) for _ in range(steps)]
+
+    def call(i, events=None):
+        k, v = pools[i % n_pools]
+        binding.decode_attn(t["q"], k, v, t["page_table"], t["ctx_lens"], t["q_lens"], t["out"],
+                            wl.scale, workspace=ws, max_ctx_len=wl.max_ctx_len, events=events)
+
+    for i in range(warmup):
+        call(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        call(warmup + i, ev[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / steps
+    kern_ms = np.array([a.elapsed_ms(b) for a, b in ev])
+    del pools, t, ws
+    torch.cuda.empty_cache()
+    qtok = int(wl.q_lens.sum())
+    return dict(workload=name, kv_bytes=kv, alg_bytes=wl.algorithmic_bytes(), ms_per_step=ms_step,
+                kernel_ms_mean=float(kern_ms.mean()), kernel_ms_median=float(np.median(kern_ms)),
+                kv_gbps=kv / (ms_step * 1e-3) / 1e9,
+                kernel_gbps=wl.algorithmic_bytes() / (kern_ms.mean() * 1e-3) / 1e9,
+                tokens_per_s=qtok / (ms_step * 1e-3), n_pools=n_pools, wl=wl)
+
+
+def cpu_baseline(wl):
+    """The float64 oracle on this host's cores over the whole bulk call."""
+    import oracle
+    from paper_2608_22788_amd import synth  # noqa: F401
+    orc = oracle.load()
+    log("[bench] cpu baseline: generating host inputs")
+    q, k, v = wl.q_values(), wl.k_pages(), wl.v_pages()
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    log(f"[bench] cpu baseline: oracle on {threads} threads")
+    t0 = time.perf_counter()
+    orc.attention(q, k, v, wl.page_table, wl.ctx_lens, wl.q_lens, wl.scale, nthreads=threads)
+    dt = time.perf_counter() - t0
+    return dict(value=wl.kv_bytes() / dt / 1e9, unit="GB/s", cores=threads, kind="oracle",
+                sample=f"whole bulk call ({wl.B} seqs, {int(wl.ctx_lens.sum())} context tokens), "
+                       f"float64, {dt:.2f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-tail", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--only", choices=list(WORKLOADS), help="time one workload only (profiling)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the attention path has no cross-GPU step; "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_22788_amd import binding
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    if args.only:
+        r = time_workload(args.only, args.steps, args.warmup)
+        r.pop("wl")
+        print(json.dumps(r), flush=True)
+        return
+
+    bulk = time_workload("bulk", args.steps, args.warmup)
+    tail = {}
+    if not args.no_tail:
+        for name in ("mtp", "dflash"):
+            r = time_workload(name, args.steps, args.warmup)
+            r.pop("wl")
+            tail[name] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
+            tail[name]["hbm_frac"] = round(r["kv_gbps"] / PEAK_GBPS, 4)
+    sweep = []
+    if not args.no_sweep:
+        log("[bench] concurrency sweep (seed 0)")
+        for p in binding.concurrency_sweep(seeds=1, warmup=5, iters=30):
+            sweep.append(dict(batch=p["batch"], q_len=p["q_len"], kv_gbps=round(p["kv_gbps"], 1),
+                              hbm_frac=round(p["hbm_frac"], 4), tokens_per_s=round(p["tokens_per_s"]),
+                              tau_us=round(p["tau_us"], 2)))
+    cpu = None if args.no_cpu_baseline else cpu_baseline(bulk["wl"])
+
+    achieved = bulk["kernel_gbps"]
+    traffic = measured_traffic("bulk")
+    line = {
+        "metric": "decode-attn KV GB/s (% of HBM peak) and tokens/s vs concurrency, bulk+tail",
+        "value": round(bulk["kv_gbps"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(bulk["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS["bulk"], "global_batch": 256, "q_len": 1,
+                   "kv_bytes_per_step": bulk["kv_bytes"], "kv_pools_rotated": bulk["n_pools"],
+                   "parallelism": "single GPU"},
+        "hbm_frac": round(bulk["kv_gbps"] / PEAK_GBPS, 4),
+        "tokens_per_s": round(bulk["tokens_per_s"]),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_GBPS, 4), "traffic": traffic,
+                     "kernel": "decode_q1_kernel<128,4>",
+                     "kernel_ms_mean": round(bulk["kernel_ms_mean"], 5),
+                     "alg_bytes_per_launch": bulk["alg_bytes"]},
+        "cpu_baseline": cpu,
+        "tail": tail,
+        "sweep_seed0": sweep,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

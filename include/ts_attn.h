@@ -1,0 +1,207 @@
+/*
+ * ts_attn.h -- C ABI of libtsattn: paged decode and speculative-verify
+ * attention for AMD Instinct MI355X (gfx950).
+ *
+ * The operation.  Rollout replicas spend their decode phase (paper Sec. 2.1)
+ * attending each sequence's new query tokens to its whole KV cache.  The bulk
+ * pool decodes one token per sequence at high concurrency; the tail pool runs
+ * speculative decoding (Sec. 3.4 and Sec. 4.3: multi-token-prediction heads
+ * with 3-5 drafts, block drafters with blocks of 4 or more) and verifies the
+ * 1 + gamma tokens of each draft block with the target model, so every
+ * sequence contributes q_len query rows that attend causally within the
+ * block.  The paper observes that long-context generation is bound by
+ * KV-cache traffic and attention memory bandwidth (App. F, speculative
+ * decoding for long context); these kernels are built to that roofline.
+ *
+ * Definition computed (fp32 accumulation, bf16 in and out):
+ *   for sequence b with L = ctx_lens[b] (L counts the q_len new tokens, whose
+ *   keys and values are already in the pages) and Q = q_lens[b]:
+ *     row i in [0, Q) sits at absolute position L - Q + i and sees keys
+ *     t in [0, L - Q + i]  (causal within the draft block, diagonal included);
+ *     query head h reads KV head h / (Hq / Hkv)  (contiguous GQA groups);
+ *     K_t = k_pages[page_table[b][t / P]][g][t % P][:], V_t likewise;
+ *     out[b][i][h][:] = sum_t softmax_t(scale * <q[b][i][h][:], K_t>) V_t.
+ *
+ * Memory layouts (row-major, all device memory unless stated):
+ *   q, out      bf16  [num_seqs][max_q_len][num_q_heads][head_dim]
+ *   k_pages,
+ *   v_pages     bf16  [num_pages][num_kv_heads][page_size][head_dim]
+ *   page_table  int32 [num_seqs][max_pages_per_seq]; entries at logical
+ *               page j >= ceil(L / P) are never read
+ *   ctx_lens,
+ *   q_lens      int32 [num_seqs]
+ *
+ * Ownership and errors.  The caller owns every buffer and the stream; the
+ * library allocates nothing inside ts_decode_attn, never synchronises it and
+ * never reads device data on the host, so a call can be captured into a HIP
+ * graph.  Inputs are read-only; out is written only at rows i < q_lens[b]
+ * (q_lens[b] = 0 skips sequence b); workspace contents are undefined on
+ * return, and concurrent calls need distinct workspaces.  Every entry point
+ * returns TS_OK (0) or a negative ts_status; on error nothing is launched and
+ * ts_last_error() describes the cause.  No C++ exception crosses the ABI.
+ *
+ * Device-side preconditions (1 <= q_lens[b] <= ctx_lens[b] <= max_ctx_len,
+ * ctx_lens[b] <= max_pages_per_seq * page_size, q_lens[b] <= max_q_len, page
+ * ids in [0, num_pages)) are the caller's to keep on the fast path; with the
+ * environment variable TS_DEBUG=1 a checking kernel verifies them first, the
+ * call synchronises and returns TS_ERR_SHAPE if any fails.
+ */
+#ifndef TS_ATTN_H
+#define TS_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TS_ATTN_ABI_VERSION 1
+
+typedef enum ts_status {
+    TS_OK = 0,
+    TS_ERR_NULL = -1,        /* a required pointer is NULL */
+    TS_ERR_SHAPE = -2,       /* shape outside the supported set, or a failed TS_DEBUG check */
+    TS_ERR_WORKSPACE = -3,   /* workspace smaller than ts_decode_attn_workspace_size() */
+    TS_ERR_UNSUPPORTED = -4, /* no device of the supported architecture */
+    TS_ERR_HIP = -5,         /* a HIP runtime call failed; see ts_last_error() */
+    TS_ERR_ARG = -6          /* an argument other than the shape is invalid */
+} ts_status;
+
+/* Host-known description of one call.  Supported: page_size 16; head_dim 64
+ * or 128; num_q_heads a multiple of num_kv_heads with group size
+ * G = num_q_heads / num_kv_heads in 1..16 and G * max_q_len <= 64;
+ * max_q_len in 1..16; num_seqs >= 1.  max_ctx_len is an upper bound on
+ * ctx_lens, used only for validation; the launch grid depends on the shape
+ * alone.  num_workers = 0 lets the library choose how many wavefronts share
+ * the KV stream; a positive value fixes it (the result does not depend on it
+ * beyond rounding; tests use it to vary the split points). */
+typedef struct ts_attn_shape {
+    int32_t num_seqs;
+    int32_t num_q_heads;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+    int32_t page_size;
+    int32_t max_q_len;
+    int32_t max_pages_per_seq;
+    int32_t max_ctx_len;
+    int64_t num_pages;
+    int32_t num_workers;
+    int32_t reserved;
+} ts_attn_shape;
+
+/* Bytes of device workspace ts_decode_attn needs for this shape (split-KV
+ * partial outputs and their log-sum-exp).  Host only; returns 0 and sets
+ * ts_last_error() for an unsupported shape. */
+size_t ts_decode_attn_workspace_size(const ts_attn_shape *shape);
+
+/* Paged decode / verify attention as defined above, enqueued on `stream`
+ * (a hipStream_t; NULL is the default stream).  `scale` multiplies the dot
+ * products (typically 1/sqrt(head_dim)).  `workspace` is device memory of at
+ * least ts_decode_attn_workspace_size(shape) bytes, 256-byte aligned. */
+int ts_decode_attn(const ts_attn_shape *shape, const void *q, const void *k_pages,
+                   const void *v_pages, const int32_t *page_table, const int32_t *ctx_lens,
+                   const int32_t *q_lens, void *out, float scale, void *workspace,
+                   size_t workspace_bytes, void *stream);
+
+/* ts_decode_attn that also records `ev_begin` just before and `ev_end` just
+ * after its main (KV-streaming) kernel on the same stream, so the caller can
+ * time that kernel alone with ts_event_elapsed_ms().  Events come from
+ * ts_event_create(); either may be NULL. */
+int ts_decode_attn_events(const ts_attn_shape *shape, const void *q, const void *k_pages,
+                          const void *v_pages, const int32_t *page_table,
+                          const int32_t *ctx_lens, const int32_t *q_lens, void *out,
+                          float scale, void *workspace, size_t workspace_bytes, void *stream,
+                          void *ev_begin, void *ev_end);
+
+/* ---- concurrency-throughput curve ------------------------------------------
+ * The paper's controller consumes a measured decode throughput v(b) versus
+ * active batch b, and the per-token time tau(b) = 1 / v(b) (Sec. 2.1;
+ * Sec. 3.2 outer loop; App. C.2).  ts_concurrency_sweep measures the
+ * attention share of that curve on this GPU: for each batch size it draws
+ * context lengths (512 + a Pareto(x_min 1024, alpha 1.5) response capped at
+ * 65536, the same SplitMix64 definitions as the test generator), a random
+ * page permutation and N(0,1) bf16 values, then times ts_decode_attn with HIP
+ * events while rotating over enough distinct KV pools to defeat the
+ * last-level cache.  Synchronous; allocates and frees its own device memory
+ * on the current device. */
+typedef struct ts_sweep_config {
+    int32_t num_q_heads;        /* 32 */
+    int32_t num_kv_heads;       /* 8 */
+    int32_t head_dim;           /* 128 */
+    int32_t num_batches;        /* entries used in batches[] */
+    int32_t batches[32];        /* e.g. 1, 2, 4, ..., 512 */
+    int32_t verify_max_batch;   /* batches <= this use q_len = verify_q_len ... */
+    int32_t verify_q_len;       /* ... (4); larger batches use q_len 1 */
+    int32_t num_seeds;          /* seeds 0 .. num_seeds-1 per batch size */
+    int32_t warmup;             /* untimed calls per point */
+    int32_t iters;              /* timed calls per point */
+    int64_t min_rotation_bytes; /* KV bytes cycled through per point (>= 1 GiB) */
+} ts_sweep_config;
+
+typedef struct ts_sweep_point {
+    int32_t batch;
+    int32_t q_len;
+    int32_t seed;
+    int32_t num_pools;          /* distinct KV pools rotated through */
+    int64_t sum_ctx;            /* sum of context lengths */
+    int64_t kv_bytes;           /* algorithmic K+V bytes per call */
+    double t_median_us;         /* per-call time, whole call (main + merge) */
+    double t_p10_us;
+    double t_p90_us;
+    double kv_gbps;             /* kv_bytes / t_median */
+    double hbm_frac;            /* kv_gbps / 8000 (MI355X HBM3E peak) */
+    double tokens_per_s;        /* batch * q_len / t_median */
+    double tau_us;              /* t_median / q_len: attention time per decoded position */
+} ts_sweep_point;
+
+/* Runs the sweep; writes up to `cap` points (num_batches * num_seeds needed)
+ * and their count to *n_out. */
+int ts_concurrency_sweep(const ts_sweep_config *cfg, ts_sweep_point *pts, int32_t cap,
+                         int32_t *n_out);
+
+/* ---- synthetic inputs (same definitions as the test generator) -------------
+ * SplitMix64 (Steele, Lea, Flood 2014) addressed by (seed, stream, index):
+ * value n = mix64(mix64((seed << 8) + stream) + (n + 1) * 0x9E3779B97F4A7C15);
+ * a bf16 value is the Box-Muller normal sqrt(-2 ln u1) cos(2 pi u2), u1 =
+ * (hi32 + 1) / 2^32, u2 = lo32 / 2^32, computed in double, rounded to float
+ * then to bf16 (nearest even). */
+
+/* Fill n bf16 values dst[i] = normal(seed, stream_id, index_offset + i) on
+ * `stream` (device memory). */
+int ts_synth_fill_bf16(void *dst, int64_t n, uint64_t seed, uint32_t stream_id,
+                       int64_t index_offset, void *stream);
+
+/* Host: context lengths of the sweep distribution for `batch` sequences. */
+int ts_synth_sweep_lengths(int32_t batch, uint64_t seed, int32_t *ctx_lens);
+
+/* Host: physical page ids for sequences of the given lengths, a uniform
+ * permutation of [0, total pages) (stable order of SplitMix64 keys), laid out
+ * [batch][max_pages_per_seq] with unused entries set to 0. */
+int ts_synth_page_table(int32_t batch, const int32_t *ctx_lens, int32_t page_size,
+                        int32_t max_pages_per_seq, uint64_t seed, int32_t *page_table);
+
+/* ---- measurement helpers ----------------------------------------------------- */
+
+/* Plain device-to-device copy kernel of `bytes` (multiple of 16, 16-byte
+ * aligned pointers); calibrates hardware byte counters against a known
+ * transfer. */
+int ts_copy_bytes(void *dst, const void *src, size_t bytes, void *stream);
+
+int ts_event_create(void **ev);
+int ts_event_destroy(void *ev);
+int ts_event_record(void *ev, void *stream);
+/* Waits for `stop` and returns the time from `start` to `stop` in ms. */
+int ts_event_elapsed_ms(void *start, void *stop, float *ms);
+
+/* ---- diagnostics ------------------------------------------------------------ */
+const char *ts_status_string(int status);
+/* Message of the last failing call on this thread ("" if none). */
+const char *ts_last_error(void);
+int ts_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TS_ATTN_H */

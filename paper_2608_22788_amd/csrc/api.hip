@@ -1,0 +1,272 @@
+// api.hip -- host side of libtsattn: shape validation, kernel selection,
+// the work-partition size, launches and error reporting behind the C ABI
+// declared in include/ts_attn.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "attn_common.h"
+#include "ts_attn.h"
+#include "ts_internal.h"
+
+namespace tsattn {
+
+kernel_fn decode_q1_variant(int D, int G);
+kernel_fn verify_variant(int D, int NB);
+kernel_fn merge_variant(int D);
+int debug_check(const ts_attn_shape *s, const int32_t *page_table, const int32_t *ctx_lens,
+                const int32_t *q_lens, hipStream_t stream);
+
+static thread_local std::string g_last_error;
+
+int fail(int status, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return status;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(TS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Device architecture check, once per device.
+int check_device() {
+    static std::mutex mu;
+    static int known[64] = {0};   // 0 unknown, 1 ok, -1 unsupported
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= 64)
+        return fail(TS_ERR_UNSUPPORTED, "device index %d out of range", dev);
+    std::lock_guard<std::mutex> lock(mu);
+    if (known[dev] == 0) {
+        hipDeviceProp_t prop;
+        e = hipGetDeviceProperties(&prop, dev);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipGetDeviceProperties");
+        known[dev] = (std::strncmp(prop.gcnArchName, "gfx950", 6) == 0) ? 1 : -1;
+        if (known[dev] < 0)
+            return fail(TS_ERR_UNSUPPORTED, "device %d is %s; this library is built for gfx950",
+                        dev, prop.gcnArchName);
+    }
+    if (known[dev] < 0)
+        return fail(TS_ERR_UNSUPPORTED, "device %d is not gfx950", dev);
+    return TS_OK;
+}
+
+struct Plan {
+    bool q1;          // one-token VALU kernel, else the matrix-core verify kernel
+    int G, NB, rows_per_unit, W;
+    size_t ws_o_bytes, ws_lse_off, ws_bytes;
+};
+
+// Number of wavefronts sharing the KV stream.  MI355X has 256 compute units;
+// the decode kernel keeps about 8 wavefronts per unit resident and the verify
+// kernel, whose row blocks live in registers, fewer.  Small shapes get fewer
+// workers so that each has at least a few pages.
+static int auto_workers(const ts_attn_shape *s, bool q1, int NB) {
+    int per_cu = q1 ? 8 : (NB <= 2 ? 8 : 4);
+    int64_t w = 256LL * per_cu;
+    const int64_t pages_ub = (int64_t)s->num_seqs * s->num_kv_heads *
+                             ((s->max_ctx_len + kPage - 1) / kPage);
+    const int64_t by_size = (pages_ub + 7) / 8;
+    if (by_size < w)
+        w = by_size;
+    return (int)(w < 1 ? 1 : w);
+}
+
+int make_plan(const ts_attn_shape *s, Plan *pl) {
+    if (!s)
+        return fail(TS_ERR_NULL, "shape is NULL");
+    if (s->num_seqs < 1 || s->num_seqs > kMaxSeqs)
+        return fail(TS_ERR_SHAPE, "num_seqs %d outside [1, %d]", s->num_seqs, kMaxSeqs);
+    if (s->num_kv_heads < 1 || s->num_q_heads < 1 || s->num_q_heads % s->num_kv_heads)
+        return fail(TS_ERR_SHAPE, "num_q_heads %d must be a positive multiple of num_kv_heads %d",
+                    s->num_q_heads, s->num_kv_heads);
+    if (s->head_dim != 64 && s->head_dim != 128)
+        return fail(TS_ERR_SHAPE, "head_dim %d unsupported (64 or 128)", s->head_dim);
+    if (s->page_size != kPage)
+        return fail(TS_ERR_SHAPE, "page_size %d unsupported (16)", s->page_size);
+    if (s->max_q_len < 1 || s->max_q_len > 16)
+        return fail(TS_ERR_SHAPE, "max_q_len %d outside [1, 16]", s->max_q_len);
+    const int G = s->num_q_heads / s->num_kv_heads;
+    if (G > 16 || G * s->max_q_len > 64)
+        return fail(TS_ERR_SHAPE, "group size %d x max_q_len %d exceeds 64 rows per KV head", G,
+                    s->max_q_len);
+    if (s->max_pages_per_seq < 1)
+        return fail(TS_ERR_SHAPE, "max_pages_per_seq %d < 1", s->max_pages_per_seq);
+    if ((int64_t)s->num_seqs * s->max_pages_per_seq >= (1LL << 31))
+        return fail(TS_ERR_SHAPE, "num_seqs x max_pages_per_seq exceeds 2^31");
+    if (s->max_ctx_len < 1 || (int64_t)s->max_ctx_len > (int64_t)s->max_pages_per_seq * kPage)
+        return fail(TS_ERR_SHAPE, "max_ctx_len %d outside [1, max_pages_per_seq x 16]", s->max_ctx_len);
+    if (s->num_pages < 1 || s->num_pages > (1LL << 31))
+        return fail(TS_ERR_SHAPE, "num_pages %lld outside [1, 2^31]", (long long)s->num_pages);
+    if (s->num_workers < 0 || s->num_workers > (1 << 20))
+        return fail(TS_ERR_SHAPE, "num_workers %d outside [0, 2^20]", s->num_workers);
+
+    pl->G = G;
+    pl->q1 = (s->max_q_len == 1) && (G == 1 || G == 2 || G == 4 || G == 8);
+    pl->rows_per_unit = G * s->max_q_len;
+    pl->NB = (pl->rows_per_unit + 15) / 16;
+    pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->NB);
+    const size_t slots = 2 * (size_t)pl->W;
+    pl->ws_o_bytes = slots * pl->rows_per_unit * s->head_dim * sizeof(float);
+    pl->ws_lse_off = (pl->ws_o_bytes + 255) & ~(size_t)255;
+    pl->ws_bytes = pl->ws_lse_off + ((slots * pl->rows_per_unit * sizeof(float) + 255) & ~(size_t)255);
+    return TS_OK;
+}
+
+static bool debug_enabled() {
+    static int v = -1;
+    if (v < 0) {
+        const char *e = std::getenv("TS_DEBUG");
+        v = (e && e[0] == '1') ? 1 : 0;
+    }
+    return v == 1;
+}
+
+static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, const void *v_pages,
+                  const int32_t *page_table, const int32_t *ctx_lens, const int32_t *q_lens,
+                  void *out, float scale, void *workspace, size_t workspace_bytes, void *stream,
+                  void *ev_begin, void *ev_end) {
+    clear_error();
+    Plan pl;
+    int st = make_plan(s, &pl);
+    if (st)
+        return st;
+    if (!q || !k_pages || !v_pages || !page_table || !ctx_lens || !q_lens || !out)
+        return fail(TS_ERR_NULL, "a tensor pointer is NULL");
+    if (!workspace)
+        return fail(TS_ERR_NULL, "workspace is NULL (need %zu bytes)", pl.ws_bytes);
+    if (workspace_bytes < pl.ws_bytes)
+        return fail(TS_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, pl.ws_bytes);
+    if (((uintptr_t)workspace & 255) || ((uintptr_t)q & 15) || ((uintptr_t)out & 15) ||
+        ((uintptr_t)k_pages & 15) || ((uintptr_t)v_pages & 15))
+        return fail(TS_ERR_ARG, "misaligned pointer (workspace needs 256 B, tensors 16 B)");
+    if (!std::isfinite(scale))
+        return fail(TS_ERR_ARG, "scale is not finite");
+    st = check_device();
+    if (st)
+        return st;
+    hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+
+    if (debug_enabled()) {
+        st = debug_check(s, page_table, ctx_lens, q_lens, hs);
+        if (st)
+            return st;
+    }
+
+    AttnParams p;
+    p.q = static_cast<const uint16_t *>(q);
+    p.k_pages = static_cast<const uint16_t *>(k_pages);
+    p.v_pages = static_cast<const uint16_t *>(v_pages);
+    p.page_table = page_table;
+    p.ctx_lens = ctx_lens;
+    p.q_lens = q_lens;
+    p.out = static_cast<uint16_t *>(out);
+    p.ws_o = static_cast<float *>(workspace);
+    p.ws_lse = reinterpret_cast<float *>(static_cast<char *>(workspace) + pl.ws_lse_off);
+    p.B = s->num_seqs;
+    p.Hq = s->num_q_heads;
+    p.Hkv = s->num_kv_heads;
+    p.D = s->head_dim;
+    p.Qmax = s->max_q_len;
+    p.max_pages = s->max_pages_per_seq;
+    p.G = pl.G;
+    p.rows_per_unit = pl.rows_per_unit;
+    p.W = pl.W;
+    p.scale_log2 = scale * 1.4426950408889634f;
+
+    kernel_fn main_k = pl.q1 ? decode_q1_variant(p.D, pl.G) : verify_variant(p.D, pl.NB);
+    kernel_fn merge_k = merge_variant(p.D);
+    if (!main_k || !merge_k)
+        return fail(TS_ERR_UNSUPPORTED, "no kernel for head_dim %d, G %d, rows %d", p.D, pl.G,
+                    pl.rows_per_unit);
+    const size_t lds = (size_t)(p.B + 1) * sizeof(int);
+
+    hipError_t e;
+    if (ev_begin && (e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_begin), hs)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    hipLaunchKernelGGL(main_k, dim3(pl.W), dim3(kWave), lds, hs, p);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return hip_fail(e, "attention kernel launch");
+    if (ev_end && (e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_end), hs)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    const int nrb = (pl.rows_per_unit + 15) / 16;
+    const unsigned merge_blocks = (unsigned)(p.B * p.Hkv * nrb);
+    hipLaunchKernelGGL(merge_k, dim3(merge_blocks), dim3(256), lds, hs, p);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return hip_fail(e, "merge kernel launch");
+    return TS_OK;
+}
+
+}  // namespace tsattn
+
+using namespace tsattn;
+
+extern "C" {
+
+size_t ts_decode_attn_workspace_size(const ts_attn_shape *shape) {
+    clear_error();
+    Plan pl;
+    if (make_plan(shape, &pl))
+        return 0;
+    return pl.ws_bytes;
+}
+
+int ts_decode_attn(const ts_attn_shape *shape, const void *q, const void *k_pages,
+                   const void *v_pages, const int32_t *page_table, const int32_t *ctx_lens,
+                   const int32_t *q_lens, void *out, float scale, void *workspace,
+                   size_t workspace_bytes, void *stream) {
+    try {
+        return launch(shape, q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale,
+                      workspace, workspace_bytes, stream, nullptr, nullptr);
+    } catch (...) {
+        return fail(TS_ERR_HIP, "unexpected C++ exception");
+    }
+}
+
+int ts_decode_attn_events(const ts_attn_shape *shape, const void *q, const void *k_pages,
+                          const void *v_pages, const int32_t *page_table,
+                          const int32_t *ctx_lens, const int32_t *q_lens, void *out,
+                          float scale, void *workspace, size_t workspace_bytes, void *stream,
+                          void *ev_begin, void *ev_end) {
+    try {
+        return launch(shape, q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale,
+                      workspace, workspace_bytes, stream, ev_begin, ev_end);
+    } catch (...) {
+        return fail(TS_ERR_HIP, "unexpected C++ exception");
+    }
+}
+
+const char *ts_status_string(int status) {
+    switch (status) {
+    case TS_OK: return "ok";
+    case TS_ERR_NULL: return "null pointer";
+    case TS_ERR_SHAPE: return "unsupported or inconsistent shape";
+    case TS_ERR_WORKSPACE: return "workspace too small";
+    case TS_ERR_UNSUPPORTED: return "unsupported device or configuration";
+    case TS_ERR_HIP: return "HIP runtime error";
+    case TS_ERR_ARG: return "invalid argument";
+    default: return "unknown status";
+    }
+}
+
+const char *ts_last_error(void) { return g_last_error.c_str(); }
+
+int ts_version(void) { return TS_ATTN_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,268 @@
+// attn_decode.hip -- paged decode attention for one query token per sequence
+// (the bulk pool's high-concurrency decode step), VALU path.
+//
+// One wavefront streams one KV head of one sequence at a time (a segment of
+// the work partition in attn_common.h) and serves all G query heads that
+// share that KV head, so each K/V byte is fetched from HBM once per group.
+//
+// Lane layout for a 16-token page: lane = 8 * slot + part.  Token slot
+// `slot` (0..7) holds tokens slot and slot + 8 of the page; `part` (0..7)
+// holds 8 of every 64 head dimensions (d = 64c + 8 part + 0..7), so the 8
+// lanes of a slot read 128 contiguous bytes of a key row per load.
+//   * scores: v_dot2_f32_bf16 on packed bf16 pairs of K and q (fp32
+//     accumulate), then a 3-step DPP butterfly over the 8 parts;
+//   * online softmax per lane (each slot keeps its own running reference
+//     m_ref, row sum and output), in log2 units with scale * log2(e) folded
+//     into the scores; the reference is only raised when a score exceeds it
+//     by more than 8 (a factor 256), so the rescale of the accumulators is
+//     skipped by the whole wavefront on almost every page, and the result is
+//     the same up to rounding because the final normalisation uses the same
+//     reference;
+//   * P.V: the two tokens of a slot are packed as one bf16 pair per head
+//     dimension, so v_dot2_f32_bf16 multiplies a probability pair by a value
+//     pair; the row sum is accumulated from the same rounded probabilities;
+//   * at the end of a segment the 8 slots are merged with log-sum-exp
+//     weights through cross-lane shuffles.
+// Masking: only the last page of a sequence has slots past the context end;
+// their probabilities are forced to 0 and their value rows to 0, so stale
+// data (even NaN) in unused slots never reaches the output.
+#include "attn_common.h"
+
+namespace tsattn {
+
+namespace {
+
+template <int NC>
+struct PageRegs {
+    uint4 k[2][NC];
+    uint4 v[2][NC];
+};
+
+template <int D, int G>
+struct DecodeQ1 {
+    static constexpr int NC = D / 64;   // 16-byte chunks per token row per lane
+    static constexpr int NO = NC * 8;   // output dims per lane
+
+    __device__ static void load_page(const AttnParams &p, const int32_t *pt, int j, int g,
+                                     int slot, int part, PageRegs<NC> &r) {
+        const int pid = pt[j];
+        const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * D);
+        const uint16_t *kb = p.k_pages + base;
+        const uint16_t *vb = p.v_pages + base;
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+#pragma unroll
+            for (int c = 0; c < NC; c++) {
+                const int off = (slot + 8 * h) * D + 64 * c + 8 * part;
+                r.k[h][c] = *reinterpret_cast<const uint4 *>(kb + off);
+                r.v[h][c] = *reinterpret_cast<const uint4 *>(vb + off);
+            }
+        }
+    }
+
+    __device__ static void segment(const AttnParams &p, const Segment &s, int slot_id) {
+        const int lane = threadIdx.x;
+        const int slot = lane >> 3;
+        const int part = lane & 7;
+        const int b = s.b, g = s.g;
+        const int L = p.ctx_lens[b];
+        const int32_t *pt = p.page_table + (size_t)b * p.max_pages;
+
+        // query rows of the group, packed bf16 pairs
+        uint32_t qv[G][NC][4];
+#pragma unroll
+        for (int r = 0; r < G; r++) {
+            const uint16_t *qr = p.q + ((size_t)b * p.Qmax * p.Hq + (size_t)g * G + r) * D;
+#pragma unroll
+            for (int c = 0; c < NC; c++) {
+                uint4 t = *reinterpret_cast<const uint4 *>(qr + 64 * c + 8 * part);
+                qv[r][c][0] = t.x;
+                qv[r][c][1] = t.y;
+                qv[r][c][2] = t.z;
+                qv[r][c][3] = t.w;
+            }
+        }
+
+        float o[G][NO];
+        float m_ref[G], lsum[G];
+#pragma unroll
+        for (int r = 0; r < G; r++) {
+            m_ref[r] = -INFINITY;
+            lsum[r] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < NO; k++)
+                o[r][k] = 0.0f;
+        }
+
+        PageRegs<NC> cur, nxt;
+        load_page(p, pt, s.j0, g, slot, part, cur);
+        for (int j = s.j0; j < s.j1; j++) {
+            if (j + 1 < s.j1)
+                load_page(p, pt, j + 1, g, slot, part, nxt);
+
+            // scores of the two tokens of this slot, all G rows
+            float x0[G], x1[G];
+#pragma unroll
+            for (int r = 0; r < G; r++) {
+                float a = 0.0f, c1 = 0.0f;
+#pragma unroll
+                for (int c = 0; c < NC; c++) {
+                    a = dot2_bf16(cur.k[0][c].x, qv[r][c][0], a);
+                    c1 = dot2_bf16(cur.k[1][c].x, qv[r][c][0], c1);
+                    a = dot2_bf16(cur.k[0][c].y, qv[r][c][1], a);
+                    c1 = dot2_bf16(cur.k[1][c].y, qv[r][c][1], c1);
+                    a = dot2_bf16(cur.k[0][c].z, qv[r][c][2], a);
+                    c1 = dot2_bf16(cur.k[1][c].z, qv[r][c][2], c1);
+                    a = dot2_bf16(cur.k[0][c].w, qv[r][c][3], a);
+                    c1 = dot2_bf16(cur.k[1][c].w, qv[r][c][3], c1);
+                }
+                x0[r] = sum8(a) * p.scale_log2;
+                x1[r] = sum8(c1) * p.scale_log2;
+            }
+
+            const bool tail = (j + 1) * kPage > L;       // wavefront-uniform
+            const int tok0 = j * kPage + slot;
+            const bool ok0 = !tail || tok0 < L;
+            const bool ok1 = !tail || tok0 + 8 < L;
+
+            bool need = false;
+            float mx[G];
+#pragma unroll
+            for (int r = 0; r < G; r++) {
+                mx[r] = fmaxf(ok0 ? x0[r] : -INFINITY, ok1 ? x1[r] : -INFINITY);
+                need |= mx[r] > m_ref[r] + kRescaleSlack;
+            }
+            if (__any(need)) {
+#pragma unroll
+                for (int r = 0; r < G; r++) {
+                    const bool up = mx[r] > m_ref[r] + kRescaleSlack;
+                    const float alpha = up ? fast_exp2(m_ref[r] - mx[r]) : 1.0f;
+                    m_ref[r] = up ? mx[r] : m_ref[r];
+                    lsum[r] *= alpha;
+#pragma unroll
+                    for (int k = 0; k < NO; k++)
+                        o[r][k] *= alpha;
+                }
+            }
+
+            if (tail) {
+#pragma unroll
+                for (int c = 0; c < NC; c++) {
+                    if (!ok0)
+                        cur.v[0][c] = make_uint4(0, 0, 0, 0);
+                    if (!ok1)
+                        cur.v[1][c] = make_uint4(0, 0, 0, 0);
+                }
+            }
+
+            uint32_t pk[G];
+#pragma unroll
+            for (int r = 0; r < G; r++) {
+                const float p0 = ok0 ? fast_exp2(x0[r] - m_ref[r]) : 0.0f;
+                const float p1 = ok1 ? fast_exp2(x1[r] - m_ref[r]) : 0.0f;
+                pk[r] = pack_bf16x2(p0, p1);
+                lsum[r] = dot2_bf16(pk[r], 0x3F803F80u, lsum[r]);
+            }
+
+#pragma unroll
+            for (int c = 0; c < NC; c++) {
+                const uint32_t va[4] = {cur.v[0][c].x, cur.v[0][c].y, cur.v[0][c].z, cur.v[0][c].w};
+                const uint32_t vb[4] = {cur.v[1][c].x, cur.v[1][c].y, cur.v[1][c].z, cur.v[1][c].w};
+#pragma unroll
+                for (int w = 0; w < 4; w++) {
+                    // (token slot, token slot + 8) pairs for dims 2w and 2w + 1
+                    const uint32_t even = (va[w] & 0xffffu) | (vb[w] << 16);
+                    const uint32_t odd = (va[w] >> 16) | (vb[w] & 0xffff0000u);
+#pragma unroll
+                    for (int r = 0; r < G; r++) {
+                        o[r][8 * c + 2 * w] = dot2_bf16(even, pk[r], o[r][8 * c + 2 * w]);
+                        o[r][8 * c + 2 * w + 1] = dot2_bf16(odd, pk[r], o[r][8 * c + 2 * w + 1]);
+                    }
+                }
+            }
+            cur = nxt;
+        }
+
+        // merge the 8 token slots (lanes part, part + 8, ..., part + 56)
+#pragma unroll
+        for (int r = 0; r < G; r++) {
+            float M = m_ref[r];
+            M = fmaxf(M, __shfl_xor(M, 8));
+            M = fmaxf(M, __shfl_xor(M, 16));
+            M = fmaxf(M, __shfl_xor(M, 32));
+            const float a = (m_ref[r] == -INFINITY) ? 0.0f : fast_exp2(m_ref[r] - M);
+            float l = lsum[r] * a;
+            l += __shfl_xor(l, 8);
+            l += __shfl_xor(l, 16);
+            l += __shfl_xor(l, 32);
+#pragma unroll
+            for (int k = 0; k < NO; k++) {
+                float v = o[r][k] * a;
+                v += __shfl_xor(v, 8);
+                v += __shfl_xor(v, 16);
+                v += __shfl_xor(v, 32);
+                o[r][k] = v;
+            }
+            const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+            if (slot == 0) {
+                const int h = g * G + r;
+                if (s.whole) {
+                    uint16_t *dst = p.out + ((size_t)b * p.Qmax * p.Hq + h) * D;
+#pragma unroll
+                    for (int c = 0; c < NC; c++) {
+                        uint4 w4;
+                        w4.x = pack_bf16x2(o[r][8 * c + 0] * inv, o[r][8 * c + 1] * inv);
+                        w4.y = pack_bf16x2(o[r][8 * c + 2] * inv, o[r][8 * c + 3] * inv);
+                        w4.z = pack_bf16x2(o[r][8 * c + 4] * inv, o[r][8 * c + 5] * inv);
+                        w4.w = pack_bf16x2(o[r][8 * c + 6] * inv, o[r][8 * c + 7] * inv);
+                        *reinterpret_cast<uint4 *>(dst + 64 * c + 8 * part) = w4;
+                    }
+                } else {
+                    const size_t row = (size_t)slot_id * p.rows_per_unit + r;
+                    float *dst = p.ws_o + row * D;
+#pragma unroll
+                    for (int c = 0; c < NC; c++) {
+                        float4 lo = make_float4(o[r][8 * c + 0] * inv, o[r][8 * c + 1] * inv,
+                                                o[r][8 * c + 2] * inv, o[r][8 * c + 3] * inv);
+                        float4 hi = make_float4(o[r][8 * c + 4] * inv, o[r][8 * c + 5] * inv,
+                                                o[r][8 * c + 6] * inv, o[r][8 * c + 7] * inv);
+                        *reinterpret_cast<float4 *>(dst + 64 * c + 8 * part) = lo;
+                        *reinterpret_cast<float4 *>(dst + 64 * c + 8 * part + 4) = hi;
+                    }
+                    if (part == 0)
+                        p.ws_lse[row] = l > 0.0f ? M + __log2f(l) : -INFINITY;
+                }
+            }
+        }
+    }
+};
+
+template <int D, int G>
+__global__ __launch_bounds__(64) void decode_q1_kernel(AttnParams p) {
+    extern __shared__ int s_pre[];
+    page_prefix(p, s_pre);
+    const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
+    const int w = blockIdx.x;
+    const int64_t begin = worker_begin(ptot, w, p.W);
+    const int64_t end = worker_begin(ptot, w + 1, p.W);
+    for (int64_t x = begin; x < end;) {
+        const Segment s = locate(p, s_pre, x, end);
+        DecodeQ1<D, G>::segment(p, s, x == begin ? 2 * w : 2 * w + 1);
+        x = s.next;
+    }
+}
+
+}  // namespace
+
+typedef void (*kernel_fn)(AttnParams);
+
+kernel_fn decode_q1_variant(int D, int G) {
+#define TS_Q1(DD, GG) \
+    if (D == DD && G == GG) return decode_q1_kernel<DD, GG>;
+    TS_Q1(64, 1) TS_Q1(64, 2) TS_Q1(64, 4) TS_Q1(64, 8)
+    TS_Q1(128, 1) TS_Q1(128, 2) TS_Q1(128, 4) TS_Q1(128, 8)
+#undef TS_Q1
+    return nullptr;
+}
+
+}  // namespace tsattn

@@ -1,0 +1,215 @@
+// sweep.hip -- ts_concurrency_sweep: the attention share of the
+// concurrency-throughput curve v(b) and per-token time tau(b) = 1 / v(b) that
+// the paper's hierarchical controller consumes (Sec. 2.1, Sec. 3.2, App. C.2).
+//
+// For each batch size b and seed: draw the sweep's context lengths and page
+// permutation on the host, fill q/K/V on the device with the seeded
+// generator, then time ts_decode_attn with HIP events.  Calls rotate over
+// enough distinct KV pools (at least min_rotation_bytes in total) that the
+// 256 MB last-level cache cannot serve a pool from the previous call, so small
+// batches report HBM, not cache, bandwidth.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <vector>
+
+#include "ts_attn.h"
+#include "ts_internal.h"
+
+namespace tsattn {
+
+int synth_fill(void *dst, int64_t n, uint64_t seed, uint32_t stream_id, int64_t offset,
+               hipStream_t stream);
+void sweep_lengths(int32_t batch, uint64_t seed, int32_t *ctx_lens);
+int build_page_table(int32_t batch, const int32_t *ctx_lens, int32_t page_size,
+                     int32_t max_pages_per_seq, uint64_t seed, int32_t *page_table);
+
+namespace {
+
+constexpr uint32_t kStreamQ = 4, kStreamK = 5, kStreamV = 6;
+
+struct DevBuf {
+    void *p = nullptr;
+    ~DevBuf() {
+        if (p)
+            (void)hipFree(p);
+    }
+    int alloc(size_t bytes, const char *what) {
+        hipError_t e = hipMalloc(&p, bytes < 256 ? 256 : bytes);
+        return e == hipSuccess ? TS_OK : hip_fail(e, what);
+    }
+};
+
+struct Events {
+    std::vector<hipEvent_t> ev;
+    ~Events() {
+        for (hipEvent_t e : ev)
+            (void)hipEventDestroy(e);
+    }
+};
+
+struct Stream {
+    hipStream_t s = nullptr;
+    ~Stream() {
+        if (s)
+            (void)hipStreamDestroy(s);
+    }
+};
+
+double quantile(std::vector<double> v, double q) {
+    std::sort(v.begin(), v.end());
+    const double pos = q * (double)(v.size() - 1);
+    const size_t lo = (size_t)std::floor(pos);
+    const size_t hi = std::min(lo + 1, v.size() - 1);
+    return v[lo] + (pos - (double)lo) * (v[hi] - v[lo]);
+}
+
+int run_point(const ts_sweep_config &c, int32_t batch, int32_t seed, hipStream_t stream,
+              ts_sweep_point *pt) {
+    const int32_t Q = batch <= c.verify_max_batch ? c.verify_q_len : 1;
+    std::vector<int32_t> lens((size_t)batch), qlens((size_t)batch, Q);
+    sweep_lengths(batch, (uint64_t)seed, lens.data());
+    int32_t maxp = 1, maxl = 1;
+    int64_t total_pages = 0, sum_ctx = 0;
+    for (int32_t L : lens) {
+        maxp = std::max(maxp, (L + 15) / 16);
+        maxl = std::max(maxl, L);
+        total_pages += (L + 15) / 16;
+        sum_ctx += L;
+    }
+    std::vector<int32_t> table((size_t)batch * maxp);
+    int st = build_page_table(batch, lens.data(), 16, maxp, (uint64_t)seed, table.data());
+    if (st)
+        return st;
+
+    const int64_t pool_elems = total_pages * c.num_kv_heads * 16 * c.head_dim;
+    const int64_t pool_bytes = pool_elems * 2;                  // one of K or V
+    int64_t pools = (c.min_rotation_bytes + 2 * pool_bytes - 1) / (2 * pool_bytes);
+    pools = std::max<int64_t>(1, std::min<int64_t>(pools, 512));
+
+    ts_attn_shape sh = {};
+    sh.num_seqs = batch;
+    sh.num_q_heads = c.num_q_heads;
+    sh.num_kv_heads = c.num_kv_heads;
+    sh.head_dim = c.head_dim;
+    sh.page_size = 16;
+    sh.max_q_len = Q;
+    sh.max_pages_per_seq = maxp;
+    sh.max_ctx_len = maxl;
+    sh.num_pages = total_pages;
+    const size_t ws_bytes = ts_decode_attn_workspace_size(&sh);
+    if (!ws_bytes)
+        return TS_ERR_SHAPE;
+
+    DevBuf k, v, q, out, ws, dtab, dlen, dq;
+    const size_t qelems = (size_t)batch * Q * c.num_q_heads * c.head_dim;
+    if ((st = k.alloc((size_t)(pool_bytes * pools), "hipMalloc(K pools)")) ||
+        (st = v.alloc((size_t)(pool_bytes * pools), "hipMalloc(V pools)")) ||
+        (st = q.alloc(qelems * 2, "hipMalloc(q)")) || (st = out.alloc(qelems * 2, "hipMalloc(out)")) ||
+        (st = ws.alloc(ws_bytes, "hipMalloc(workspace)")) ||
+        (st = dtab.alloc(table.size() * 4, "hipMalloc(page table)")) ||
+        (st = dlen.alloc((size_t)batch * 4, "hipMalloc(ctx_lens)")) ||
+        (st = dq.alloc((size_t)batch * 4, "hipMalloc(q_lens)")))
+        return st;
+    hipError_t e;
+    if ((e = hipMemcpyAsync(dtab.p, table.data(), table.size() * 4, hipMemcpyHostToDevice, stream)) ||
+        (e = hipMemcpyAsync(dlen.p, lens.data(), (size_t)batch * 4, hipMemcpyHostToDevice, stream)) ||
+        (e = hipMemcpyAsync(dq.p, qlens.data(), (size_t)batch * 4, hipMemcpyHostToDevice, stream)))
+        return hip_fail(e, "hipMemcpyAsync(sweep inputs)");
+    if ((st = synth_fill(k.p, pool_elems * pools, (uint64_t)seed, kStreamK, 0, stream)) ||
+        (st = synth_fill(v.p, pool_elems * pools, (uint64_t)seed, kStreamV, 0, stream)) ||
+        (st = synth_fill(q.p, (int64_t)qelems, (uint64_t)seed, kStreamQ, 0, stream)))
+        return st;
+
+    const float scale = 1.0f / std::sqrt((float)c.head_dim);
+    auto call = [&](int64_t i) {
+        const size_t off = (size_t)((i % pools) * pool_bytes);
+        return ts_decode_attn(&sh, q.p, static_cast<char *>(k.p) + off, static_cast<char *>(v.p) + off,
+                              static_cast<const int32_t *>(dtab.p), static_cast<const int32_t *>(dlen.p),
+                              static_cast<const int32_t *>(dq.p), out.p, scale, ws.p, ws_bytes, stream);
+    };
+    for (int i = 0; i < c.warmup; i++)
+        if ((st = call(i)))
+            return st;
+    Events evs;
+    evs.ev.resize((size_t)c.iters + 1);
+    for (auto &ev : evs.ev)
+        if ((e = hipEventCreate(&ev)))
+            return hip_fail(e, "hipEventCreate");
+    if ((e = hipEventRecord(evs.ev[0], stream)))
+        return hip_fail(e, "hipEventRecord");
+    for (int i = 0; i < c.iters; i++) {
+        if ((st = call(c.warmup + i)))
+            return st;
+        if ((e = hipEventRecord(evs.ev[(size_t)i + 1], stream)))
+            return hip_fail(e, "hipEventRecord");
+    }
+    if ((e = hipStreamSynchronize(stream)))
+        return hip_fail(e, "hipStreamSynchronize");
+    std::vector<double> us((size_t)c.iters);
+    for (int i = 0; i < c.iters; i++) {
+        float ms = 0.f;
+        if ((e = hipEventElapsedTime(&ms, evs.ev[(size_t)i], evs.ev[(size_t)i + 1])))
+            return hip_fail(e, "hipEventElapsedTime");
+        us[(size_t)i] = 1000.0 * ms;
+    }
+    pt->batch = batch;
+    pt->q_len = Q;
+    pt->seed = seed;
+    pt->num_pools = (int32_t)pools;
+    pt->sum_ctx = sum_ctx;
+    pt->kv_bytes = sum_ctx * c.num_kv_heads * c.head_dim * 2 * 2;
+    pt->t_median_us = quantile(us, 0.5);
+    pt->t_p10_us = quantile(us, 0.1);
+    pt->t_p90_us = quantile(us, 0.9);
+    pt->kv_gbps = (double)pt->kv_bytes / (pt->t_median_us * 1e-6) / 1e9;
+    pt->hbm_frac = pt->kv_gbps / 8000.0;
+    pt->tokens_per_s = (double)batch * Q / (pt->t_median_us * 1e-6);
+    pt->tau_us = pt->t_median_us / Q;
+    return TS_OK;
+}
+
+}  // namespace
+}  // namespace tsattn
+
+using namespace tsattn;
+
+extern "C" int ts_concurrency_sweep(const ts_sweep_config *cfg, ts_sweep_point *pts, int32_t cap,
+                                    int32_t *n_out) {
+    clear_error();
+    if (!cfg || !pts || !n_out)
+        return fail(TS_ERR_NULL, "NULL argument");
+    const ts_sweep_config &c = *cfg;
+    if (c.num_batches < 1 || c.num_batches > 32 || c.num_seeds < 1 || c.iters < 1 || c.warmup < 0)
+        return fail(TS_ERR_ARG, "invalid batch list, seed count or iteration counts");
+    for (int i = 0; i < c.num_batches; i++)
+        if (c.batches[i] < 1 || c.batches[i] > 4096)
+            return fail(TS_ERR_ARG, "batch size %d outside [1, 4096]", c.batches[i]);
+    if (c.verify_q_len < 1 || c.verify_q_len > 16 || c.min_rotation_bytes < 0)
+        return fail(TS_ERR_ARG, "invalid verify_q_len or rotation size");
+    if ((int64_t)c.num_batches * c.num_seeds > cap)
+        return fail(TS_ERR_ARG, "cap %d < %d points", cap, c.num_batches * c.num_seeds);
+    int st = check_device();
+    if (st)
+        return st;
+    try {
+        Stream s;
+        hipError_t e = hipStreamCreate(&s.s);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipStreamCreate");
+        int32_t n = 0;
+        for (int i = 0; i < c.num_batches; i++) {
+            for (int seed = 0; seed < c.num_seeds; seed++) {
+                st = run_point(c, c.batches[i], seed, s.s, &pts[n]);
+                if (st)
+                    return st;
+                n++;
+            }
+        }
+        *n_out = n;
+        return TS_OK;
+    } catch (...) {
+        return fail(TS_ERR_HIP, "out of host memory");
+    }
+}

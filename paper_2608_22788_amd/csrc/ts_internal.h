@@ -1,0 +1,20 @@
+// ts_internal.h -- host-side helpers shared by the library's translation
+// units (error reporting, device check).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tsattn {
+
+struct AttnParams;
+typedef void (*kernel_fn)(AttnParams);
+
+// Records a formatted message as the thread's last error and returns status.
+int fail(int status, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int hip_fail(hipError_t e, const char *what);
+void clear_error();
+// TS_OK if the current device is a gfx950, else TS_ERR_UNSUPPORTED / TS_ERR_HIP.
+int check_device();
+
+}  // namespace tsattn

@@ -32,8 +32,11 @@ implement the same definitions independently; tests check that they agree.
 """
 from __future__ import annotations
 
+import ctypes
 import dataclasses
 import math
+import os
+import subprocess
 from typing import Dict, Optional, Sequence
 
 import numpy as np
@@ -120,12 +123,47 @@ def normal_bf16(seed: int, stream: int, index) -> np.ndarray:
     return f32_to_bf16_bits(x.astype(np.float32))
 
 
-def normal_bf16_range(seed: int, stream: int, start: int, count: int,
-                      chunk: int = 1 << 22) -> np.ndarray:
+def normal_bf16_range_numpy(seed: int, stream: int, start: int, count: int,
+                            chunk: int = 1 << 22) -> np.ndarray:
     out = np.empty(count, dtype=np.uint16)
     for s in range(0, count, chunk):
         n = min(chunk, count - s)
         out[s:s + n] = normal_bf16(seed, stream, np.arange(start + s, start + s + n, dtype=np.uint64))
+    return out
+
+
+_HOST_SRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "synth_host.c")
+_HOST_LIB = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtssynth.so")
+_host = None
+
+
+def build_host(out: str = _HOST_LIB) -> str:
+    """Compile the OpenMP C version of the value generator (gcc)."""
+    subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC",
+                    "-shared", _HOST_SRC, "-o", out + ".tmp", "-lm"], check=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+def _host_lib():
+    global _host
+    if _host is None and os.path.exists(_HOST_LIB):
+        lib = ctypes.CDLL(_HOST_LIB)
+        lib.ts_synth_normal_bf16_host.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64,
+                                                  ctypes.c_int64, ctypes.c_void_p]
+        lib.ts_synth_normal_bf16_host.restype = None
+        _host = lib
+    return _host
+
+
+def normal_bf16_range(seed: int, stream: int, start: int, count: int) -> np.ndarray:
+    """bf16 bits of draws [start, start + count) of a stream (C if built)."""
+    lib = _host_lib()
+    if lib is None:
+        return normal_bf16_range_numpy(seed, stream, start, count)
+    out = np.empty(count, dtype=np.uint16)
+    if count:
+        lib.ts_synth_normal_bf16_host(seed, stream, start, count, out.ctypes.data)
     return out
 
 

@@ -1,0 +1,236 @@
+"""Parity of the HIP path (through the C ABI) with the float64 oracle.
+
+Small cases compare every output element; the full-size workloads compare
+every row of sampled sequences (the longest, the shortest and random others)
+computed in the same launch configuration the benchmark times, plus
+properties that hold at any size (finite outputs, untouched canaries)."""
+import numpy as np
+import pytest
+
+from paper_2608_22788_amd import synth
+
+from gpu_util import assert_parity, canary_ok, oracle_out, sample_seqs, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2608_22788_amd import binding, device
+    return binding, device
+
+
+def small_cfg(Hq, Hkv, D):
+    return dict(B=1, Hq=Hq, Hkv=Hkv, D=D, q_len=1, lengths=("uniform", 1, 1), scale=1.0 / np.sqrt(D))
+
+
+def test_device_fill_matches_host_generator(dev):
+    import torch
+    binding, _ = dev
+    for seed, stream, off, n in [(0, synth.S_K, 0, 1 << 22), (5, synth.S_V, 987654321, 1 << 20 | 7),
+                                 (2, synth.S_Q, 3, 1001)]:
+        say(f"fill seed={seed} stream={stream} off={off} n={n}")
+        t = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+        binding.synth_fill(t, seed, stream, off)
+        got = t.view(torch.int16).cpu().numpy().view(np.uint16)
+        want = synth.normal_bf16_range(seed, stream, off, n)
+        assert np.array_equal(got, want)
+
+
+def run_case(dev, orc, wl, workers=(0,), values="host"):
+    _, device = dev
+    ref = oracle_out(orc, wl)
+    t = device.upload(wl, values=values)
+    for w in workers:
+        say(f"case {wl.name} B={wl.B} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} Qmax={wl.Qmax} "
+            f"lens={list(wl.ctx_lens)[:8]} q={list(wl.q_lens)[:8]} workers={w}")
+        device.run(wl, t, num_workers=w)
+        got = device.out_as_f64(t)
+        assert_parity(got, ref, f"{wl.name}/w{w}")
+        canary_ok(t, wl)
+    return t, ref
+
+
+def test_tiny_config(dev, orc):
+    wl = synth.make_workload("tiny", seed=0, poison=True, spare_pages=3)
+    run_case(dev, orc, wl, workers=(0, 1, 2, 7, 64))
+
+
+GRID = [
+    # (Hq, Hkv, D, q_lens, ctx_lens)
+    (8, 2, 64, [1, 1, 1], [16, 17, 300]),
+    (32, 8, 128, [1] * 5, [1, 15, 16, 33, 1000]),
+    (8, 8, 128, [1, 1], [47, 2048]),
+    (16, 2, 128, [1, 1, 1], [64, 65, 511]),
+    (4, 4, 64, [2, 2], [2, 80]),
+    (32, 8, 128, [4] * 3, [4, 31, 777]),
+    (32, 8, 128, [3, 3], [19, 260]),
+    (32, 8, 128, [5, 6], [100, 6]),
+    (32, 8, 128, [16, 16], [16, 1500]),
+    (32, 8, 64, [16, 7], [40, 333]),
+    (16, 1, 128, [4, 4], [48, 129]),
+    (32, 8, 128, [4, 1, 0, 4], [64, 50, 30, 97]),     # ragged, one sequence skipped
+    (8, 2, 128, [1, 0, 1], [20, 5, 700]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(GRID)))
+def test_small_grid(dev, orc, case):
+    Hq, Hkv, D, ql, cl = GRID[case]
+    wl = synth.make_workload(f"grid{case}", seed=100 + case, cfg=small_cfg(Hq, Hkv, D), ctx_lens=cl,
+                             q_lens=ql, poison=True, spare_pages=2)
+    run_case(dev, orc, wl, workers=(0, 1, 3, 40))
+
+
+def test_one_key_returns_value_row_bitwise(dev, orc):
+    _, device = dev
+    for Qmax in (1, 2):
+        wl = synth.make_workload("onekey", seed=9, cfg=small_cfg(32, 8, 128), ctx_lens=[1, 1, 1],
+                                 q_lens=[1, 1, 1], Qmax=Qmax)
+        t = device.upload(wl)
+        device.run(wl, t)
+        out = t["out"].view(__import__("torch").int16).cpu().numpy().view(np.uint16)
+        vp = wl.v_pages()
+        for b in range(3):
+            for h in range(32):
+                assert np.array_equal(out[b, 0, h], vp[wl.page_table[b, 0], h // 4, 0]), (Qmax, b, h)
+
+
+def test_constant_values_give_exactly_that_value(dev):
+    import torch
+    _, device = dev
+    for q in (1, 4, 16):
+        wl = synth.make_workload("constv", seed=4, cfg=small_cfg(32, 8, 128), ctx_lens=[q + 40, 3000],
+                                 q_lens=[q, q])
+        t = device.upload(wl, values="device")
+        t["v_pages"].fill_(1.0)
+        device.run(wl, t)
+        got = device.out_as_f64(t)
+        assert (got[:, :q] == 1.0).all(), q
+
+
+def test_page_relabel_is_bitwise_invariant(dev):
+    import torch
+    _, device = dev
+    wl = synth.make_workload("relabel", seed=5, cfg=small_cfg(32, 8, 128), ctx_lens=[100, 3001, 64],
+                             q_lens=[4, 4, 2])
+    t = device.upload(wl)
+    device.run(wl, t)
+    base = t["out"].clone()
+    perm = torch.from_numpy(np.random.default_rng(0).permutation(wl.num_pages)).cuda()
+    k2 = torch.empty_like(t["k_pages"])
+    v2 = torch.empty_like(t["v_pages"])
+    k2[perm] = t["k_pages"]
+    v2[perm] = t["v_pages"]
+    t["k_pages"], t["v_pages"] = k2, v2
+    t["page_table"] = perm[t["page_table"].long()].int().contiguous()
+    device.run(wl, t)
+    assert torch.equal(t["out"].view(torch.int16), base.view(torch.int16))
+
+
+def test_run_to_run_bitwise_deterministic(dev):
+    import torch
+    _, device = dev
+    for name in ("tiny", "mtp"):
+        wl = synth.make_workload(name, seed=1)
+        t = device.upload(wl, values="device")
+        device.run(wl, t)
+        first = t["out"].clone()
+        for _ in range(2):
+            device.run(wl, t)
+            assert torch.equal(t["out"].view(torch.int16), first.view(torch.int16)), name
+
+
+def test_verify_rows_equal_prefix_decodes(dev, orc):
+    import torch
+    _, device = dev
+    L, Q = 2000, 6
+    wl = synth.make_workload("vp", seed=6, cfg=small_cfg(32, 8, 128), ctx_lens=[L], q_lens=[Q])
+    t = device.upload(wl)
+    device.run(wl, t)
+    full = device.out_as_f64(t)
+    for i in range(Q):
+        one = synth.make_workload("vp1", seed=6, cfg=small_cfg(32, 8, 128), ctx_lens=[L - Q + i + 1],
+                                  q_lens=[1])
+        t1 = device.upload(one)
+        t1["k_pages"], t1["v_pages"] = t["k_pages"], t["v_pages"]
+        t1["page_table"] = t["page_table"]
+        t1["q"] = t["q"][:, i:i + 1].contiguous()
+        device.run(one, t1, workspace=None)
+        got = device.out_as_f64(t1)
+        assert_parity(got[0, 0][None, None], full[0, i][None, None], f"row{i}")
+
+
+def test_split_points_do_not_change_the_result(dev):
+    import torch
+    _, device = dev
+    wl = synth.make_workload("split", seed=2, cfg=synth.CONFIGS["dflash"], ctx_lens=[20000, 333],
+                             q_lens=[16, 16])
+    t = device.upload(wl, values="device")
+    outs = []
+    for w in (1, 2, 7, 0, 300):
+        device.run(wl, t, num_workers=w)
+        outs.append(device.out_as_f64(t))
+    for o in outs[1:]:
+        assert_parity(o, outs[0], "split")
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads, sampled against the oracle
+# ---------------------------------------------------------------------------
+
+FULL = {"bulk": 6, "mtp": 3, "dflash": 2}
+
+
+@pytest.mark.parametrize("name", list(FULL))
+def test_full_size_config(dev, orc, name):
+    _, device = dev
+    wl = synth.make_workload(name, seed=0)
+    say(f"full {name}: B={wl.B} sum_ctx={int(wl.ctx_lens.sum())} max={wl.max_ctx_len} "
+        f"KV={wl.kv_bytes() / 1e9:.2f} GB")
+    t = device.upload(wl, values="device")
+    device.run(wl, t)
+    got = device.out_as_f64(t)
+    canary_ok(t, wl)
+    assert np.isfinite(got).all()
+    seqs = sample_seqs(wl, FULL[name])
+    sub = wl.subset(seqs)
+    ref = oracle_out(orc, sub)
+    assert_parity(got[seqs], ref, f"{name} seqs {seqs}")
+
+
+SWEEP_CASES = [(b, 0) for b in synth.SWEEP_BATCHES] + \
+              [(b, s) for b in synth.SWEEP_BATCHES if b <= 64 for s in range(1, 5)]
+
+
+@pytest.mark.parametrize("batch,seed", SWEEP_CASES)
+def test_sweep_workload(dev, orc, batch, seed):
+    _, device = dev
+    wl = synth.make_workload(f"sweep_b{batch}", seed=seed)
+    say(f"sweep b={batch} seed={seed}: q_len={wl.Qmax} sum_ctx={int(wl.ctx_lens.sum())}")
+    t = device.upload(wl, values="device")
+    device.run(wl, t)
+    got = device.out_as_f64(t)
+    canary_ok(t, wl)
+    assert np.isfinite(got).all()
+    seqs = sample_seqs(wl, 3 if batch > 8 else batch, seed)
+    ref = oracle_out(orc, wl.subset(seqs))
+    assert_parity(got[seqs], ref, f"sweep b{batch} s{seed}")
+
+
+def test_concurrency_sweep_entry_point(dev):
+    binding, _ = dev
+    pts = binding.concurrency_sweep(batches=(1, 16, 128), seeds=2, warmup=2, iters=10,
+                                    min_rotation_bytes=1 << 30)
+    assert len(pts) == 6
+    for p in pts:
+        say(f"  sweep point {p}")
+        assert p["q_len"] == (4 if p["batch"] <= 8 else 1)
+        lens = synth.lengths_sweep(p["seed"], p["batch"])
+        assert p["sum_ctx"] == int(lens.sum())
+        assert p["kv_bytes"] == int(lens.sum()) * 8 * 128 * 4
+        assert p["num_pools"] * p["kv_bytes"] >= (1 << 30)
+        assert 0 < p["t_p10_us"] <= p["t_median_us"] <= p["t_p90_us"]
+        assert p["kv_gbps"] > 0 and p["hbm_frac"] < 1.2
