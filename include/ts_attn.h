@@ -73,9 +73,19 @@ typedef enum ts_status {
  * G = num_q_heads / num_kv_heads in 1..16 and G * max_q_len <= 64;
  * max_q_len in 1..16; num_seqs >= 1.  max_ctx_len is an upper bound on
  * ctx_lens, used only for validation; the launch grid depends on the shape
- * alone.  num_workers = 0 lets the library choose how many wavefronts share
- * the KV stream; a positive value fixes it (the result does not depend on it
- * beyond rounding; tests use it to vary the split points). */
+ * alone.  num_workers = 0 lets the library choose how many workers (one
+ * wavefront, or a four-wavefront team for verify at head_dim 128) share the
+ * KV stream; a positive value fixes it (the result does not depend on it
+ * beyond rounding; tests use it to vary the split points).  variant selects
+ * the kernel for max_q_len > 1: TS_VARIANT_AUTO, TS_VARIANT_WAVE (one
+ * wavefront holds every row block) or TS_VARIANT_TEAM (head_dim 128 only:
+ * four wavefronts share each page through LDS); it is ignored for
+ * max_q_len == 1 with a group size of 1, 2, 4 or 8, which always uses the
+ * one-token decode kernel. */
+#define TS_VARIANT_AUTO 0
+#define TS_VARIANT_WAVE 1
+#define TS_VARIANT_TEAM 2
+
 typedef struct ts_attn_shape {
     int32_t num_seqs;
     int32_t num_q_heads;
@@ -87,7 +97,7 @@ typedef struct ts_attn_shape {
     int32_t max_ctx_len;
     int64_t num_pages;
     int32_t num_workers;
-    int32_t reserved;
+    int32_t variant;
 } ts_attn_shape;
 
 /* Bytes of device workspace ts_decode_attn needs for this shape (split-KV

@@ -28,7 +28,10 @@ class AttnShape(ctypes.Structure):
                 ("page_size", ctypes.c_int32), ("max_q_len", ctypes.c_int32),
                 ("max_pages_per_seq", ctypes.c_int32), ("max_ctx_len", ctypes.c_int32),
                 ("num_pages", ctypes.c_int64), ("num_workers", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("variant", ctypes.c_int32)]
+
+
+VARIANT_AUTO, VARIANT_WAVE, VARIANT_TEAM = 0, 1, 2
 
 
 class SweepConfig(ctypes.Structure):
@@ -120,9 +123,9 @@ def check(status: int, where: str) -> None:
 
 
 def make_shape(num_seqs, num_q_heads, num_kv_heads, head_dim, max_q_len, max_pages_per_seq,
-               max_ctx_len, num_pages, num_workers=0, page_size=16) -> AttnShape:
+               max_ctx_len, num_pages, num_workers=0, page_size=16, variant=0) -> AttnShape:
     return AttnShape(num_seqs, num_q_heads, num_kv_heads, head_dim, page_size, max_q_len,
-                     max_pages_per_seq, max_ctx_len, num_pages, num_workers, 0)
+                     max_pages_per_seq, max_ctx_len, num_pages, num_workers, variant)
 
 
 def workspace_size(shape: AttnShape) -> int:
@@ -138,13 +141,13 @@ def _stream_ptr(stream) -> int:
     return int(s.cuda_stream)
 
 
-def shape_of(q, k_pages, page_table, max_ctx_len=None, num_workers=0) -> AttnShape:
+def shape_of(q, k_pages, page_table, max_ctx_len=None, num_workers=0, variant=0) -> AttnShape:
     B, Qmax, Hq, D = q.shape
     NP, Hkv, P, D2 = k_pages.shape
     assert D == D2, "q and k_pages head_dim differ"
     maxp = page_table.shape[1]
     return make_shape(B, Hq, Hkv, D, Qmax, maxp, maxp * P if max_ctx_len is None else int(max_ctx_len),
-                      NP, num_workers, P)
+                      NP, num_workers, P, variant)
 
 
 def _check_tensors(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out):
@@ -161,14 +164,14 @@ def _check_tensors(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out):
 
 def decode_attn(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale: float,
                 workspace=None, max_ctx_len: Optional[int] = None, num_workers: int = 0,
-                stream=None, events=None):
+                stream=None, events=None, variant: int = 0):
     """ts_decode_attn on torch tensors; returns the workspace tensor used.
 
     ``events`` = (begin, end) handles from ``Event`` to time the main kernel.
     """
     import torch
     _check_tensors(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out)
-    shape = shape_of(q, k_pages, page_table, max_ctx_len, num_workers)
+    shape = shape_of(q, k_pages, page_table, max_ctx_len, num_workers, variant)
     need = workspace_size(shape)
     if workspace is None or workspace.numel() * workspace.element_size() < need:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)

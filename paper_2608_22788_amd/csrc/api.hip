@@ -19,6 +19,7 @@ namespace tsattn {
 
 kernel_fn decode_q1_variant(int D, int G);
 kernel_fn verify_variant(int D, int NB);
+kernel_fn verify_team_variant(int rows, int *lds_bytes, int *nbe);
 kernel_fn merge_variant(int D);
 int debug_check(const ts_attn_shape *s, const int32_t *page_table, const int32_t *ctx_lens,
                 const int32_t *q_lens, hipStream_t stream);
@@ -68,17 +69,22 @@ int check_device() {
 }
 
 struct Plan {
-    bool q1;          // one-token VALU kernel, else the matrix-core verify kernel
+    bool q1;          // one-token VALU kernel, else a matrix-core verify kernel
+    bool team;        // verify by four-wavefront teams sharing pages in LDS (head_dim 128)
     int G, NB, rows_per_unit, W;
     size_t ws_o_bytes, ws_lse_off, ws_bytes;
 };
 
-// Number of wavefronts sharing the KV stream.  MI355X has 256 compute units;
-// the decode kernel keeps about 8 wavefronts per unit resident and the verify
-// kernel, whose row blocks live in registers, fewer.  Small shapes get fewer
-// workers so that each has at least a few pages.
-static int auto_workers(const ts_attn_shape *s, bool q1, int NB) {
-    int per_cu = q1 ? 8 : (NB <= 2 ? 8 : 4);
+// Number of workers sharing the KV stream.  MI355X has 256 compute units.
+// Measured on the bulk, MTP and block-draft workloads: the decode kernel is
+// best with 4 single-wavefront workers per unit (1024 in all; 2048 and 4096
+// are within 3 %), the team verify kernel with 1 (one row block) or 2
+// workgroups per unit.  Fewer workers also mean fewer split partials to merge.
+// Small shapes get fewer workers so that each has at least a few pages.
+static int auto_workers(const ts_attn_shape *s, bool q1, bool team, int NB) {
+    // Team kernels with one row block run one workgroup per compute unit (their
+    // register use allows one wavefront per SIMD); with 2 or 4 row blocks, two.
+    int per_cu = q1 ? 4 : team ? (NB == 1 ? 1 : 2) : (NB <= 2 ? 8 : 4);
     int64_t w = 256LL * per_cu;
     const int64_t pages_ub = (int64_t)s->num_seqs * s->num_kv_heads *
                              ((s->max_ctx_len + kPage - 1) / kPage);
@@ -116,12 +122,17 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
         return fail(TS_ERR_SHAPE, "num_pages %lld outside [1, 2^31]", (long long)s->num_pages);
     if (s->num_workers < 0 || s->num_workers > (1 << 20))
         return fail(TS_ERR_SHAPE, "num_workers %d outside [0, 2^20]", s->num_workers);
+    if (s->variant < TS_VARIANT_AUTO || s->variant > TS_VARIANT_TEAM)
+        return fail(TS_ERR_SHAPE, "variant %d unknown", s->variant);
+    if (s->variant == TS_VARIANT_TEAM && s->head_dim != 128)
+        return fail(TS_ERR_SHAPE, "the team verify kernel needs head_dim 128");
 
     pl->G = G;
     pl->q1 = (s->max_q_len == 1) && (G == 1 || G == 2 || G == 4 || G == 8);
     pl->rows_per_unit = G * s->max_q_len;
     pl->NB = (pl->rows_per_unit + 15) / 16;
-    pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->NB);
+    pl->team = !pl->q1 && s->head_dim == 128 && s->variant != TS_VARIANT_WAVE;
+    pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team, pl->NB);
     const size_t slots = 2 * (size_t)pl->W;
     pl->ws_o_bytes = slots * pl->rows_per_unit * s->head_dim * sizeof(float);
     pl->ws_lse_off = (pl->ws_o_bytes + 255) & ~(size_t)255;
@@ -190,24 +201,36 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
     p.W = pl.W;
     p.scale_log2 = scale * 1.4426950408889634f;
 
-    kernel_fn main_k = pl.q1 ? decode_q1_variant(p.D, pl.G) : verify_variant(p.D, pl.NB);
+    const size_t lds = (size_t)(p.B + 1) * sizeof(int);
+    kernel_fn main_k = nullptr;
+    size_t main_lds = lds;
+    int main_threads = kWave;
+    if (pl.q1) {
+        main_k = decode_q1_variant(p.D, pl.G);
+    } else if (pl.team) {
+        int extra = 0, nbe = 0;
+        main_k = verify_team_variant(pl.rows_per_unit, &extra, &nbe);
+        main_lds = ((lds + 15) & ~(size_t)15) + (size_t)extra;
+        main_threads = 4 * kWave;
+    } else {
+        main_k = verify_variant(p.D, pl.NB);
+    }
     kernel_fn merge_k = merge_variant(p.D);
     if (!main_k || !merge_k)
         return fail(TS_ERR_UNSUPPORTED, "no kernel for head_dim %d, G %d, rows %d", p.D, pl.G,
                     pl.rows_per_unit);
-    const size_t lds = (size_t)(p.B + 1) * sizeof(int);
 
     hipError_t e;
     if (ev_begin && (e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_begin), hs)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    hipLaunchKernelGGL(main_k, dim3(pl.W), dim3(kWave), lds, hs, p);
+    hipLaunchKernelGGL(main_k, dim3(pl.W), dim3(main_threads), main_lds, hs, p);
     if ((e = hipGetLastError()) != hipSuccess)
         return hip_fail(e, "attention kernel launch");
     if (ev_end && (e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_end), hs)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
-    const int nrb = (pl.rows_per_unit + 15) / 16;
-    const unsigned merge_blocks = (unsigned)(p.B * p.Hkv * nrb);
-    hipLaunchKernelGGL(merge_k, dim3(merge_blocks), dim3(256), lds, hs, p);
+    const int ngroups = (pl.rows_per_unit + 3) / 4;
+    const unsigned merge_blocks = (unsigned)(p.B * p.Hkv * ngroups);
+    hipLaunchKernelGGL(merge_k, dim3(merge_blocks), dim3(kWave), lds, hs, p);
     if ((e = hipGetLastError()) != hipSuccess)
         return hip_fail(e, "merge kernel launch");
     return TS_OK;

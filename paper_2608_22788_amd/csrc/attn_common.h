@@ -91,14 +91,24 @@ __device__ __forceinline__ float sum8(float x) {
 
 __device__ __forceinline__ int first_lane_int(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Metadata (page table, context and draft lengths) is read-only for the whole
+// launch.  Reading it through the constant address space lets wavefront-uniform
+// reads become scalar loads, which are counted separately from the vector
+// loads of K/V pages; a vector load here would make the wavefront wait for
+// every K/V prefetch still in flight before it could compute the next address.
+typedef const int32_t __attribute__((address_space(4))) *const_i32_ptr;
+__device__ __forceinline__ int32_t ld_meta(const int32_t *p, size_t i) {
+    return ((const_i32_ptr)p)[i];
+}
+
 // ---------------------------------------------------------------------------
 // Work partition (see the header comment).
 // ---------------------------------------------------------------------------
 
 // Pages of sequence b that carry work: 0 if q_lens[b] == 0.
 __device__ __forceinline__ int seq_pages(const AttnParams &p, int b) {
-    int L = p.ctx_lens[b];
-    int Q = p.q_lens[b];
+    int L = ld_meta(p.ctx_lens, b);
+    int Q = ld_meta(p.q_lens, b);
     return (Q > 0 && L > 0) ? (L + kPage - 1) / kPage : 0;
 }
 

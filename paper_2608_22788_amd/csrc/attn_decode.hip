@@ -45,7 +45,7 @@ struct DecodeQ1 {
 
     __device__ static void load_page(const AttnParams &p, const int32_t *pt, int j, int g,
                                      int slot, int part, PageRegs<NC> &r) {
-        const int pid = pt[j];
+        const int pid = ld_meta(pt, j);
         const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * D);
         const uint16_t *kb = p.k_pages + base;
         const uint16_t *vb = p.v_pages + base;
@@ -65,7 +65,7 @@ struct DecodeQ1 {
         const int slot = lane >> 3;
         const int part = lane & 7;
         const int b = s.b, g = s.g;
-        const int L = p.ctx_lens[b];
+        const int L = ld_meta(p.ctx_lens, b);
         const int32_t *pt = p.page_table + (size_t)b * p.max_pages;
 
         // query rows of the group, packed bf16 pairs
@@ -94,11 +94,13 @@ struct DecodeQ1 {
                 o[r][k] = 0.0f;
         }
 
+        // The prefetch of page j + 1 is issued unconditionally (the last page of
+        // the segment is simply loaded again at the end): a load under a branch
+        // would make the compiler wait for it before computing page j.
         PageRegs<NC> cur, nxt;
         load_page(p, pt, s.j0, g, slot, part, cur);
         for (int j = s.j0; j < s.j1; j++) {
-            if (j + 1 < s.j1)
-                load_page(p, pt, j + 1, g, slot, part, nxt);
+            load_page(p, pt, min(j + 1, s.j1 - 1), g, slot, part, nxt);
 
             // scores of the two tokens of this slot, all G rows
             float x0[G], x1[G];

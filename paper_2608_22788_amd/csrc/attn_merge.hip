@@ -3,24 +3,48 @@
 //
 // For a row with partials (o_s, lse_s), lse in log2 units:
 //   M = max_s lse_s,  w_s = 2^(lse_s - M),  out = sum_s w_s o_s / sum_s w_s,
-// and a split that saw no visible key (lse = -inf) has weight 0.  The slots
-// are visited in worker order, so the result is deterministic.  One block
-// of 256 threads handles 16 rows of one unit: thread (row, part) owns D/16
-// consecutive dims of one row.
+// and a split that saw no visible key (lse = -inf) has weight 0.  Partials
+// are visited in worker order, so the result is deterministic.
+//
+// One wavefront handles 4 rows of one unit: lane (row, part) owns D/16
+// consecutive dims of one row.  The partial slots of a unit are found by
+// walking its workers once (workers with an empty range wrote nothing and are
+// skipped); the walk is wavefront-uniform.  Loads of up to kBatch partials
+// are issued before any is consumed, so the merge costs a few memory
+// latencies rather than one per partial.
 #include "attn_common.h"
 
 namespace tsattn {
 
 namespace {
 
+constexpr int kBatch = 8;   // partials in flight per lane
+
+struct SlotWalk {
+    int64_t ptot, us, wb;
+    int w, whi, W;
+    // Next up to kBatch slots; returns how many.
+    __device__ int next(int *slots) {
+        int n = 0;
+        while (n < kBatch && w <= whi) {
+            const int64_t we = worker_begin(ptot, w + 1, W);
+            if (we > wb)
+                slots[n++] = wb >= us ? 2 * w : 2 * w + 1;
+            wb = we;
+            w++;
+        }
+        return n;
+    }
+};
+
 template <int D>
-__global__ __launch_bounds__(256) void merge_kernel(AttnParams p) {
+__global__ __launch_bounds__(64) void merge_kernel(AttnParams p) {
     extern __shared__ int s_pre[];
     page_prefix(p, s_pre);
     constexpr int VE = D / 16;
-    const int nrb = (p.rows_per_unit + 15) / 16;
-    const int unit = blockIdx.x / nrb;
-    const int rb = blockIdx.x % nrb;
+    const int ngroups = (p.rows_per_unit + 3) / 4;
+    const int unit = blockIdx.x / ngroups;
+    const int rg = blockIdx.x % ngroups;
     const int b = unit / p.Hkv;
     const int g = unit % p.Hkv;
     const int np = s_pre[b + 1] - s_pre[b];
@@ -34,47 +58,66 @@ __global__ __launch_bounds__(256) void merge_kernel(AttnParams p) {
     if (wlo == whi)
         return;   // one worker saw the whole unit and wrote `out` itself
 
-    const int r = rb * 16 + (threadIdx.x >> 4);
-    const int part = threadIdx.x & 15;
-    const int Q = p.q_lens[b];
-    if (r >= p.rows_per_unit || r / p.G >= Q)
-        return;
+    const int lane = threadIdx.x;
+    const int r = rg * 4 + (lane >> 4);
+    const int part = lane & 15;
+    const int Q = ld_meta(p.q_lens, b);
+    const bool row_ok = r < p.rows_per_unit && r / p.G < Q;
+    const int rr = row_ok ? r : 0;   // keep addresses inside the workspace
 
-    // Workers with an empty range (more workers than pages) wrote nothing.
+    // pass 1: the largest log-sum-exp of the row
     float M = -INFINITY;
-    for (int w = wlo; w <= whi; w++) {
-        const int64_t wb = worker_begin(ptot, w, p.W);
-        if (worker_begin(ptot, w + 1, p.W) == wb)
-            continue;
-        const int slot = wb >= us ? 2 * w : 2 * w + 1;
-        M = fmaxf(M, p.ws_lse[(size_t)slot * p.rows_per_unit + r]);
+    {
+        SlotWalk walk{ptot, us, worker_begin(ptot, wlo, p.W), wlo, whi, p.W};
+        int slots[kBatch];
+        for (int n; (n = walk.next(slots)) > 0;) {
+            float l[kBatch];
+#pragma unroll
+            for (int k = 0; k < kBatch; k++)
+                l[k] = k < n ? p.ws_lse[(size_t)slots[k] * p.rows_per_unit + rr] : -INFINITY;
+#pragma unroll
+            for (int k = 0; k < kBatch; k++)
+                M = fmaxf(M, l[k]);
+        }
     }
+
+    // pass 2: weighted sum of the normalised partials
     float acc[VE];
 #pragma unroll
     for (int e = 0; e < VE; e++)
         acc[e] = 0.0f;
     float den = 0.0f;
-    for (int w = wlo; w <= whi; w++) {
-        const int64_t wb = worker_begin(ptot, w, p.W);
-        if (worker_begin(ptot, w + 1, p.W) == wb)
-            continue;
-        const int slot = wb >= us ? 2 * w : 2 * w + 1;
-        const size_t row = (size_t)slot * p.rows_per_unit + r;
-        const float lse = p.ws_lse[row];
-        if (lse == -INFINITY)
-            continue;
-        const float wt = fast_exp2(lse - M);
-        den += wt;
-        const float *src = p.ws_o + row * D + VE * part;
+    {
+        SlotWalk walk{ptot, us, worker_begin(ptot, wlo, p.W), wlo, whi, p.W};
+        int slots[kBatch];
+        for (int n; (n = walk.next(slots)) > 0;) {
+            float l[kBatch];
+            float4 v[kBatch][VE / 4];
 #pragma unroll
-        for (int e = 0; e < VE; e += 4) {
-            const float4 v = *reinterpret_cast<const float4 *>(src + e);
-            acc[e] += wt * v.x;
-            acc[e + 1] += wt * v.y;
-            acc[e + 2] += wt * v.z;
-            acc[e + 3] += wt * v.w;
+            for (int k = 0; k < kBatch; k++) {
+                const size_t row = (size_t)(k < n ? slots[k] : slots[0]) * p.rows_per_unit + rr;
+                l[k] = k < n ? p.ws_lse[row] : -INFINITY;
+                const float *src = p.ws_o + row * D + VE * part;
+#pragma unroll
+                for (int e = 0; e < VE / 4; e++)
+                    v[k][e] = *reinterpret_cast<const float4 *>(src + 4 * e);
+            }
+#pragma unroll
+            for (int k = 0; k < kBatch; k++) {
+                const float wt = l[k] == -INFINITY ? 0.0f : fast_exp2(l[k] - M);
+                den += wt;
+#pragma unroll
+                for (int e = 0; e < VE / 4; e++) {
+                    acc[4 * e + 0] += wt * v[k][e].x;
+                    acc[4 * e + 1] += wt * v[k][e].y;
+                    acc[4 * e + 2] += wt * v[k][e].z;
+                    acc[4 * e + 3] += wt * v[k][e].w;
+                }
+            }
         }
     }
+    if (!row_ok)
+        return;
     const float inv = den > 0.0f ? 1.0f / den : 0.0f;
     const int i = r / p.G;
     uint16_t *dst = p.out + (((size_t)b * p.Qmax + i) * p.Hq + (size_t)g * p.G + r % p.G) * D + VE * part;

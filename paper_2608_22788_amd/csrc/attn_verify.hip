@@ -5,27 +5,27 @@
 // The G query heads of a KV group times the q_len draft rows form
 // R = G * Qmax rows per (sequence, KV head) unit, padded to NB blocks of 16;
 // row r is draft position i = r / G of query head g * G + r % G.  One
-// wavefront streams the unit's pages two at a time (32 tokens) and keeps
-// every row block in registers, so each K/V byte is read once for all rows.
+// wavefront streams the unit's pages and keeps every row block in registers,
+// so each K/V byte is read once for all rows of the group.
 //
-// With l = lane, n = l % 16, kq = l / 16, and v_mfma_f32_16x16x32_bf16
-// operand layouts (A: row l%16, k 8(l/16)..+7; B: col l%16, k 8(l/16)..+7;
-// C: row 4(l/16)+i, col l%16):
-//   * scores S^T = K Q^T per page: A = 16 key rows x 32 dims loaded straight
-//     from the page (16 bytes per lane), B = Q^T kept in registers.  Lane
-//     (n, kq) receives tokens 4kq..4kq+3 of the page for query row n;
-//   * probabilities P = exp2(scale*log2e * S - m_ref) are packed to bf16 in
-//     the lane that computed them and used directly as the A operand of
-//     O = P V, with the contraction index k = 8kq + e standing for token
-//     16(e/4) + 4kq + e%4 of the page pair;
-//   * V is loaded as rows (lane (n, kq) reads D/16 consecutive dims of its 8
-//     tokens) and transposed in registers with byte permutes, so the B
-//     operand of the j-th P.V product holds dims (D/16) n + j;
+// With l = lane, n = l % 16, kq = l / 16, per 16-token page:
+//   * scores S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (A: row l%16, k
+//     8(l/16)..+7; B: col l%16, k 8(l/16)..+7; C: row 4(l/16)+i, col l%16):
+//     A = 16 key rows x 32 dims loaded straight from the page (16 bytes per
+//     lane), B = Q^T kept in registers.  Lane (n, kq) receives tokens
+//     4kq..4kq+3 of the page for query row n;
+//   * probabilities P = exp2(scale*log2e * S - m_ref), packed to bf16 in the
+//     lane that computed them, are exactly the A operand of O = P V on
+//     v_mfma_f32_16x16x16_bf16 (A: row l%16, k 4(l/16)..+3);
+//   * V is loaded as rows (lane (n, kq) reads D/16 consecutive dims of tokens
+//     4kq..4kq+3) and transposed in registers, so the B operand of the j-th
+//     P.V product holds dims (D/16) n + j of those four tokens;
 //   * row sums come from one more product of P with a ones operand, so they
 //     use exactly the rounded probabilities that weight V;
 //   * the running reference m_ref of each row is only raised when a score
 //     exceeds it by more than 8 in log2 units, which leaves the accumulators
-//     untouched on almost every page pair.
+//     untouched on almost every page;
+//   * pages are prefetched kRing - 1 ahead into a ring of registers.
 // Masks: key t is visible to draft row i iff t <= L - Q + i; keys past the
 // segment end or the context end get probability 0 and their value rows are
 // zeroed before the product, so stale data never reaches the output.
@@ -35,13 +35,10 @@ namespace tsattn {
 
 namespace {
 
-template <int D>
-struct VerifyTypes {
-    static constexpr int KS = D / 32;   // k-steps of the score product
-    static constexpr int VE = D / 16;   // value dims per lane (= P.V products per row block)
-};
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8_t, u); }
+__device__ __forceinline__ s16x4_t as_s16x4(uint2 u) { return __builtin_bit_cast(s16x4_t, u); }
 
 template <int VE>
 struct VRow;
@@ -66,38 +63,27 @@ struct VRow<4> {
 
 template <int D, int NB>
 struct Verify {
-    static constexpr int KS = VerifyTypes<D>::KS;
-    static constexpr int VE = VerifyTypes<D>::VE;
+    static constexpr int KS = D / 32;   // k-steps of the score product
+    static constexpr int VE = D / 16;   // value dims per lane = P.V products per row block
+    static constexpr int kRing = 2;   // pages in the register ring
 
-    struct PairRegs {
-        uint4 k[2][KS];        // A operands of the score product, per page
-        VRow<VE> v[2][4];      // value rows of the lane's 8 tokens
+    struct PageRegs {
+        uint4 k[KS];        // A operands of the score product
+        VRow<VE> v[4];      // value rows of the lane's 4 tokens
     };
 
-    __device__ static void load_pair(const AttnParams &p, const int32_t *pt, int jp, bool has2,
-                                     int g, int n, int kq, PairRegs &r) {
+    __device__ static void load_page(const AttnParams &p, const int32_t *pt, int j, int g, int n,
+                                     int kq, PageRegs &r) {
+        const int pid = ld_meta(pt, j);
+        const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * D);
+        const uint16_t *kb = p.k_pages + base + (size_t)n * D + 8 * kq;
 #pragma unroll
-        for (int pg = 0; pg < 2; pg++) {
-            if (pg == 1 && !has2) {
+        for (int s = 0; s < KS; s++)
+            r.k[s] = *reinterpret_cast<const uint4 *>(kb + 32 * s);
+        const uint16_t *vb = p.v_pages + base + (size_t)(4 * kq) * D + VE * n;
 #pragma unroll
-                for (int s = 0; s < KS; s++)
-                    r.k[1][s] = make_uint4(0, 0, 0, 0);
-#pragma unroll
-                for (int i = 0; i < 4; i++)
-                    r.v[1][i].zero();
-                continue;
-            }
-            const int pid = pt[jp + pg];
-            const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * D);
-            const uint16_t *kb = p.k_pages + base + (size_t)n * D + 8 * kq;
-#pragma unroll
-            for (int s = 0; s < KS; s++)
-                r.k[pg][s] = *reinterpret_cast<const uint4 *>(kb + 32 * s);
-            const uint16_t *vb = p.v_pages + base + (size_t)(4 * kq) * D + VE * n;
-#pragma unroll
-            for (int i = 0; i < 4; i++)
-                r.v[pg][i].load(vb + (size_t)i * D);
-        }
+        for (int i = 0; i < 4; i++)
+            r.v[i].load(vb + (size_t)i * D);
     }
 
     // Element e (0..VE-1) of a VE-wide bf16 row held in dwords.
@@ -106,132 +92,124 @@ struct Verify {
         return (e & 1) ? (w >> 16) : (w & 0xffffu);
     }
 
+    struct State {
+        uint4 qf[NB][KS];
+        int lim[NB];
+        f32x4_t acc[NB][VE];
+        f32x4_t lacc[NB];
+        float m_ref[NB];
+    };
+
+    __device__ static void page_step(const AttnParams &p, State &st, PageRegs &cur, int j,
+                                     int full_end, int seg_end_tok, int kq) {
+        const int t0 = j * kPage;
+        const bool masked = t0 + kPage > full_end;          // wavefront-uniform
+        if (t0 + kPage > seg_end_tok) {
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+                if (t0 + 4 * kq + i >= seg_end_tok)
+                    cur.v[i].zero();
+        }
+        // transpose the lane's 4 value rows: vt[jj] = dim (VE n + jj) of its 4 tokens
+        uint2 vt[VE];
+#pragma unroll
+        for (int jj = 0; jj < VE; jj++)
+            vt[jj] = make_uint2(half_of(cur.v[0], jj) | (half_of(cur.v[1], jj) << 16),
+                                half_of(cur.v[2], jj) | (half_of(cur.v[3], jj) << 16));
+        const uint2 ones = make_uint2(0x3F803F80u, 0x3F803F80u);
+
+#pragma unroll
+        for (int rb = 0; rb < NB; rb++) {
+            f32x4_t sc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ks++)
+                sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cur.k[ks]), as_bf16x8(st.qf[rb][ks]),
+                                                             sc, 0, 0, 0);
+            float x[4];
+            bool ok[4];
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                x[e] = sc[e] * p.scale_log2;
+                ok[e] = !masked || (t0 + 4 * kq + e < st.lim[rb]);
+            }
+            float mx = fmaxf(fmaxf(ok[0] ? x[0] : -INFINITY, ok[1] ? x[1] : -INFINITY),
+                             fmaxf(ok[2] ? x[2] : -INFINITY, ok[3] ? x[3] : -INFINITY));
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const bool up = mx > st.m_ref[rb] + kRescaleSlack;
+            if (__any(up)) {
+                const float alpha = up ? fast_exp2(st.m_ref[rb] - mx) : 1.0f;
+                st.m_ref[rb] = up ? mx : st.m_ref[rb];
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const float ai = __shfl(alpha, 4 * kq + i);
+                    st.lacc[rb][i] *= ai;
+#pragma unroll
+                    for (int jj = 0; jj < VE; jj++)
+                        st.acc[rb][jj][i] *= ai;
+                }
+            }
+            const float p0 = ok[0] ? fast_exp2(x[0] - st.m_ref[rb]) : 0.0f;
+            const float p1 = ok[1] ? fast_exp2(x[1] - st.m_ref[rb]) : 0.0f;
+            const float p2 = ok[2] ? fast_exp2(x[2] - st.m_ref[rb]) : 0.0f;
+            const float p3 = ok[3] ? fast_exp2(x[3] - st.m_ref[rb]) : 0.0f;
+            const s16x4_t pa = as_s16x4(make_uint2(pack_bf16x2(p0, p1), pack_bf16x2(p2, p3)));
+            st.lacc[rb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, as_s16x4(ones), st.lacc[rb], 0, 0, 0);
+#pragma unroll
+            for (int jj = 0; jj < VE; jj++)
+                st.acc[rb][jj] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, as_s16x4(vt[jj]),
+                                                                           st.acc[rb][jj], 0, 0, 0);
+        }
+    }
+
     __device__ static void segment(const AttnParams &p, const Segment &s, int slot_id) {
         const int lane = threadIdx.x;
         const int n = lane & 15;
         const int kq = lane >> 4;
         const int b = s.b, g = s.g;
         const int G = p.G;
-        const int L = p.ctx_lens[b];
-        const int Q = p.q_lens[b];
+        const int L = ld_meta(p.ctx_lens, b);
+        const int Q = ld_meta(p.q_lens, b);
         const int R = p.rows_per_unit;
         const int32_t *pt = p.page_table + (size_t)b * p.max_pages;
         const int seg_end_tok = min(L, s.j1 * kPage);
 
-        // query fragments (B operand of the score product) and causal limits
-        uint4 qf[NB][KS];
-        int lim[NB];
+        State st;
 #pragma unroll
         for (int rb = 0; rb < NB; rb++) {
             const int r = rb * 16 + n;
             const bool row_ok = r < R && r / G < Q;
             const int i = row_ok ? r / G : 0;
             const int hl = row_ok ? r % G : 0;
-            lim[rb] = min(row_ok ? L - Q + i + 1 : L, seg_end_tok);
+            st.lim[rb] = min(row_ok ? L - Q + i + 1 : L, seg_end_tok);
             const uint16_t *qr = p.q + (((size_t)b * p.Qmax + i) * p.Hq + (size_t)g * G + hl) * D + 8 * kq;
 #pragma unroll
             for (int ks = 0; ks < KS; ks++)
-                qf[rb][ks] = row_ok ? *reinterpret_cast<const uint4 *>(qr + 32 * ks) : make_uint4(0, 0, 0, 0);
+                st.qf[rb][ks] = row_ok ? *reinterpret_cast<const uint4 *>(qr + 32 * ks) : make_uint4(0, 0, 0, 0);
+            st.m_ref[rb] = -INFINITY;
+            st.lacc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int jj = 0; jj < VE; jj++)
+                st.acc[rb][jj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
         // keys below this bound are visible to every row of the block
         const int full_end = min(L - Q + 1, seg_end_tok);
 
-        f32x4_t acc[NB][VE];
-        f32x4_t lacc[NB];
-        float m_ref[NB];
+        // Prefetches are issued unconditionally with the page index clamped to
+        // the segment: a load under a branch would make the compiler wait for
+        // it before the current page is computed.
+        PageRegs ring[kRing];
 #pragma unroll
-        for (int rb = 0; rb < NB; rb++) {
-            m_ref[rb] = -INFINITY;
-            lacc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int k = 0; k < kRing - 1; k++)
+            load_page(p, pt, min(s.j0 + k, s.j1 - 1), g, n, kq, ring[k]);
+        for (int j = s.j0; j < s.j1; j += kRing) {
 #pragma unroll
-            for (int jj = 0; jj < VE; jj++)
-                acc[rb][jj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        }
-        const uint4 ones4 = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
-
-        PairRegs cur, nxt;
-        load_pair(p, pt, s.j0, s.j0 + 1 < s.j1, g, n, kq, cur);
-        for (int jp = s.j0; jp < s.j1; jp += 2) {
-            if (jp + 2 < s.j1)
-                load_pair(p, pt, jp + 2, jp + 3 < s.j1, g, n, kq, nxt);
-            const int t0 = jp * kPage;                   // first token of the pair
-            const bool masked = t0 + 2 * kPage > full_end;  // wavefront-uniform
-
-            // value rows of keys past the segment / context end become 0
-            if (t0 + 2 * kPage > seg_end_tok) {
-#pragma unroll
-                for (int pg = 0; pg < 2; pg++)
-#pragma unroll
-                    for (int i = 0; i < 4; i++)
-                        if (t0 + 16 * pg + 4 * kq + i >= seg_end_tok)
-                            cur.v[pg][i].zero();
+            for (int k = 0; k < kRing; k++) {
+                if (j + k < s.j1) {
+                    load_page(p, pt, min(j + k + kRing - 1, s.j1 - 1), g, n, kq, ring[(k + kRing - 1) % kRing]);
+                    page_step(p, st, ring[k], j + k, full_end, seg_end_tok, kq);
+                }
             }
-
-            // transpose the lane's 8 value rows: vt[jj] = dim (VE n + jj) of tokens k = 0..7
-            uint4 vt[VE];
-#pragma unroll
-            for (int jj = 0; jj < VE; jj++) {
-                uint32_t w[4];
-#pragma unroll
-                for (int q2 = 0; q2 < 4; q2++) {
-                    const int pg = q2 >> 1, i0 = 2 * (q2 & 1);
-                    w[q2] = half_of(cur.v[pg][i0], jj) | (half_of(cur.v[pg][i0 + 1], jj) << 16);
-                }
-                vt[jj] = make_uint4(w[0], w[1], w[2], w[3]);
-            }
-
-#pragma unroll
-            for (int rb = 0; rb < NB; rb++) {
-                f32x4_t sc[2];
-#pragma unroll
-                for (int pg = 0; pg < 2; pg++) {
-                    sc[pg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int ks = 0; ks < KS; ks++)
-                        sc[pg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cur.k[pg][ks]),
-                                                                         as_bf16x8(qf[rb][ks]), sc[pg], 0, 0, 0);
-                }
-                float x[8];
-                bool ok[8];
-#pragma unroll
-                for (int e = 0; e < 8; e++) {
-                    x[e] = sc[e >> 2][e & 3] * p.scale_log2;
-                    ok[e] = !masked || (t0 + 16 * (e >> 2) + 4 * kq + (e & 3) < lim[rb]);
-                }
-                float mx = -INFINITY;
-#pragma unroll
-                for (int e = 0; e < 8; e++)
-                    mx = fmaxf(mx, ok[e] ? x[e] : -INFINITY);
-                mx = fmaxf(mx, __shfl_xor(mx, 16));
-                mx = fmaxf(mx, __shfl_xor(mx, 32));
-                const bool up = mx > m_ref[rb] + kRescaleSlack;
-                if (__any(up)) {
-                    const float alpha = up ? fast_exp2(m_ref[rb] - mx) : 1.0f;
-                    m_ref[rb] = up ? mx : m_ref[rb];
-#pragma unroll
-                    for (int i = 0; i < 4; i++) {
-                        const float ai = __shfl(alpha, 4 * kq + i);
-                        lacc[rb][i] *= ai;
-#pragma unroll
-                        for (int jj = 0; jj < VE; jj++)
-                            acc[rb][jj][i] *= ai;
-                    }
-                }
-                uint32_t pw[4];
-#pragma unroll
-                for (int q2 = 0; q2 < 4; q2++) {
-                    const int e0 = 2 * q2, e1 = 2 * q2 + 1;
-                    const float p0 = ok[e0] ? fast_exp2(x[e0] - m_ref[rb]) : 0.0f;
-                    const float p1 = ok[e1] ? fast_exp2(x[e1] - m_ref[rb]) : 0.0f;
-                    pw[q2] = pack_bf16x2(p0, p1);
-                }
-                const bf16x8_t pa = as_bf16x8(make_uint4(pw[0], pw[1], pw[2], pw[3]));
-                lacc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, as_bf16x8(ones4), lacc[rb], 0, 0, 0);
-#pragma unroll
-                for (int jj = 0; jj < VE; jj++)
-                    acc[rb][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, as_bf16x8(vt[jj]), acc[rb][jj], 0, 0, 0);
-            }
-            cur = nxt;
         }
 
         // epilogue: lane holds rows 16 rb + 4 kq + i, dims VE n .. VE n + VE - 1
@@ -240,8 +218,8 @@ struct Verify {
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 const int r = rb * 16 + 4 * kq + i;
-                const float m = __shfl(m_ref[rb], 4 * kq + i);
-                const float l = lacc[rb][i];
+                const float m = __shfl(st.m_ref[rb], 4 * kq + i);
+                const float l = st.lacc[rb][i];
                 const int di = r / G;
                 if (r >= R || di >= Q)
                     continue;
@@ -251,7 +229,7 @@ struct Verify {
                     uint32_t w[VE / 2];
 #pragma unroll
                     for (int e = 0; e < VE / 2; e++)
-                        w[e] = pack_bf16x2(acc[rb][2 * e][i] * inv, acc[rb][2 * e + 1][i] * inv);
+                        w[e] = pack_bf16x2(st.acc[rb][2 * e][i] * inv, st.acc[rb][2 * e + 1][i] * inv);
                     if constexpr (VE == 8)
                         *reinterpret_cast<uint4 *>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
                     else
@@ -262,8 +240,8 @@ struct Verify {
 #pragma unroll
                     for (int e = 0; e < VE; e += 4)
                         *reinterpret_cast<float4 *>(dst + e) =
-                            make_float4(acc[rb][e][i] * inv, acc[rb][e + 1][i] * inv,
-                                        acc[rb][e + 2][i] * inv, acc[rb][e + 3][i] * inv);
+                            make_float4(st.acc[rb][e][i] * inv, st.acc[rb][e + 1][i] * inv,
+                                        st.acc[rb][e + 2][i] * inv, st.acc[rb][e + 3][i] * inv);
                     if (n == 0)
                         p.ws_lse[row] = l > 0.0f ? m + __log2f(l) : -INFINITY;
                 }

@@ -1,0 +1,412 @@
+// attn_verify_team.hip -- speculative-verify attention (head_dim 128) by a
+// team of four wavefronts that share each KV page through LDS.
+//
+// Rows.  The G query heads of a KV group times the Qmax draft rows form
+// R = G * Qmax rows per (sequence, KV head) unit, in NBE blocks of 16
+// (NBE = 1, 2 or 4; R padded up).  Row r is draft position r / G of query
+// head g * G + r % G.  Wave w owns row block w % NBE of page w / NBE of each
+// group of PS = 4 / NBE consecutive pages, so with 64 rows the four waves
+// split the rows of one page and with 16 rows they take four pages each.
+// A workgroup is one worker of the stream-K partition (attn_common.h).
+//
+// Staging.  A page is eight 1 KiB slabs: four K slabs (slab s holds, for
+// consumer lane l = 16 kq + n, key row n dims 32 s + 8 kq .. + 7: the A
+// operand of the score product) and four V slabs (slab i holds value row
+// 4 kq + i dims 8 n .. 8 n + 7).  Each lane loads the 16 bytes that the same
+// lane of every consumer wave will read, so global loads are coalesced row
+// segments and LDS reads are conflict-free consecutive 16-byte lanes.  The
+// four waves split the loading; loads run kDepth groups ahead in registers,
+// are written into one of two LDS stages, and one barrier per page group
+// separates writing a stage from reading it.
+//
+// Math per page and row block (l = lane, n = l % 16, kq = l / 16):
+//   S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (lane gets tokens 4kq..4kq+3 of
+//   row n); P = exp2(scale log2e S - m_ref) packed to bf16 in the same lane
+//   is the A operand of O += P V on v_mfma_f32_16x16x16_bf16; V rows are
+//   transposed in registers; row sums are P times a ones operand; m_ref is
+//   raised only when a score exceeds it by more than 8 (log2 units).
+// At the end of a segment the PS waves of a row block merge their running
+// states through LDS with log-sum-exp weights; the first one writes.
+// Masks: key t is visible to draft row i iff t <= L - Q + i; keys past the
+// segment or context end get probability 0 and zeroed value rows.
+#include "attn_common.h"
+
+#include <type_traits>
+
+namespace tsattn {
+
+namespace {
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t u) { return __builtin_bit_cast(bf16x8_t, u); }
+__device__ __forceinline__ u32x4_t ld16(const void *p) { return *reinterpret_cast<const u32x4_t *>(p); }
+__device__ __forceinline__ s16x4_t as_s16x4(uint2 u) { return __builtin_bit_cast(s16x4_t, u); }
+
+// Calls f(std::integral_constant<int, I>) for I = B .. E - 1 (compile-time).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+// Wait for this wave's LDS operations, then meet the other waves.
+// Release/acquire fences limited to LDS keep outstanding global prefetches in
+// flight across the barrier (only lgkmcnt is waited for).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+constexpr int kD = 128;
+constexpr int kSlab = 1024;               // bytes per slab
+constexpr int kPageLds = 8 * kSlab;       // one page in fragment order
+constexpr int kTeam = 4;                  // wavefronts per workgroup
+
+template <int NBE>
+struct Team {
+    static constexpr int PS = kTeam / NBE;        // pages per group
+    static constexpr int SLABS = 8 * PS;          // slabs per group
+    static constexpr int PER_WAVE = SLABS / kTeam;  // slabs each wave loads per group
+    static constexpr int STAGE = PS * kPageLds;   // LDS bytes per stage
+    static constexpr int kDepth = NBE == 1 ? 2 : 4;  // groups in flight in registers
+
+    struct Regs {
+        u32x4_t s[PER_WAVE];
+    };
+    // kDepth register sets addressed only by compile-time index.
+    struct Ring {
+        Regs r0, r1, r2, r3;
+        template <int K>
+        __device__ __forceinline__ Regs &at() {
+            static_assert(K >= 0 && K < 4, "ring slot");
+            if constexpr (K == 0) return r0;
+            else if constexpr (K == 1) return r1;
+            else if constexpr (K == 2) return r2;
+            else return r3;
+        }
+    };
+
+    // Issue this wave's loads of group `grp` (pages j0 + grp * PS + po).  Pages
+    // past the segment are clamped to its last page rather than skipped: a load
+    // under a branch would make the compiler wait for it at the join.
+    __device__ __forceinline__ static void load_group(const AttnParams &p, const int32_t *pt, int g, int j0, int j1,
+                                      int grp, int wave, int lane, Regs &r) {
+        const int n = lane & 15, kq = lane >> 4;
+#pragma unroll
+        for (int t = 0; t < PER_WAVE; t++) {
+            const int tau = wave + kTeam * t;
+            const int po = tau >> 3, sl = tau & 7;
+            const int j = min(j0 + grp * PS + po, j1 - 1);
+            const int pid = ld_meta(pt, j);
+            const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * kD);
+            const size_t off = sl < 4 ? (size_t)n * kD + 32 * sl + 8 * kq
+                                      : (size_t)(4 * kq + sl - 4) * kD + 8 * n;
+            const uint16_t *src = (sl < 4 ? p.k_pages : p.v_pages) + base + off;
+            r.s[t] = ld16(src);
+        }
+    }
+
+    __device__ __forceinline__ static void store_group(char *stage, int wave, int lane, const Regs &r) {
+#pragma unroll
+        for (int t = 0; t < PER_WAVE; t++) {
+            const int tau = wave + kTeam * t;
+            *reinterpret_cast<u32x4_t *>(stage + tau * kSlab + lane * 16) = r.s[t];
+        }
+    }
+
+    struct State {
+        u32x4_t qf[4];
+        int lim;
+        f32x4_t acc[8];
+        f32x4_t lacc;
+        float m_ref;
+    };
+
+    __device__ __forceinline__ static void page_step(const AttnParams &p, State &st, const char *pg, int j,
+                                     int full_end, int seg_end_tok, int lane) {
+        const int kq = lane >> 4;
+        u32x4_t kf[4], vr[4];
+#pragma unroll
+        for (int s = 0; s < 4; s++)
+            kf[s] = ld16(pg + s * kSlab + lane * 16);
+#pragma unroll
+        for (int i = 0; i < 4; i++)
+            vr[i] = ld16(pg + (4 + i) * kSlab + lane * 16);
+        const int t0 = j * kPage;
+        const bool masked = t0 + kPage > full_end;            // wavefront-uniform
+        if (t0 + kPage > seg_end_tok) {
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+                if (t0 + 4 * kq + i >= seg_end_tok)
+                    vr[i] = u32x4_t{0u, 0u, 0u, 0u};
+        }
+        // transpose: vt[jj] = dim 8 n + jj of tokens 4kq .. 4kq + 3
+        const uint32_t v0[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
+        const uint32_t v1[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
+        const uint32_t v2[4] = {vr[2].x, vr[2].y, vr[2].z, vr[2].w};
+        const uint32_t v3[4] = {vr[3].x, vr[3].y, vr[3].z, vr[3].w};
+        uint2 vt[8];
+#pragma unroll
+        for (int w = 0; w < 4; w++) {
+            vt[2 * w] = make_uint2((v0[w] & 0xffffu) | (v1[w] << 16), (v2[w] & 0xffffu) | (v3[w] << 16));
+            vt[2 * w + 1] = make_uint2((v0[w] >> 16) | (v1[w] & 0xffff0000u),
+                                       (v2[w] >> 16) | (v3[w] & 0xffff0000u));
+        }
+
+        f32x4_t sc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 4; s++)
+            sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[s]), as_bf16x8(st.qf[s]), sc, 0, 0, 0);
+        float x[4];
+        bool ok[4];
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            x[e] = sc[e] * p.scale_log2;
+            ok[e] = !masked || (t0 + 4 * kq + e < st.lim);
+        }
+        float mx = fmaxf(fmaxf(ok[0] ? x[0] : -INFINITY, ok[1] ? x[1] : -INFINITY),
+                         fmaxf(ok[2] ? x[2] : -INFINITY, ok[3] ? x[3] : -INFINITY));
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const bool up = mx > st.m_ref + kRescaleSlack;
+        if (__any(up)) {
+            const float alpha = up ? fast_exp2(st.m_ref - mx) : 1.0f;
+            st.m_ref = up ? mx : st.m_ref;
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const float ai = __shfl(alpha, 4 * kq + i);
+                st.lacc[i] *= ai;
+#pragma unroll
+                for (int jj = 0; jj < 8; jj++)
+                    st.acc[jj][i] *= ai;
+            }
+        }
+        const float p0 = ok[0] ? fast_exp2(x[0] - st.m_ref) : 0.0f;
+        const float p1 = ok[1] ? fast_exp2(x[1] - st.m_ref) : 0.0f;
+        const float p2 = ok[2] ? fast_exp2(x[2] - st.m_ref) : 0.0f;
+        const float p3 = ok[3] ? fast_exp2(x[3] - st.m_ref) : 0.0f;
+        const s16x4_t pa = as_s16x4(make_uint2(pack_bf16x2(p0, p1), pack_bf16x2(p2, p3)));
+        const uint2 ones = make_uint2(0x3F803F80u, 0x3F803F80u);
+        st.lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, as_s16x4(ones), st.lacc, 0, 0, 0);
+#pragma unroll
+        for (int jj = 0; jj < 8; jj++)
+            st.acc[jj] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, as_s16x4(vt[jj]), st.acc[jj], 0, 0, 0);
+    }
+
+    // Per-wave merge record in LDS (for waves po > 0).
+    struct Rec {
+        float acc[8][4][64];    // [jj][i][lane]
+        float lacc[4][64];
+        float m[16];
+    };
+
+    __device__ __forceinline__ static void segment(const AttnParams &p, const Segment &s, int slot_id, char *lds) {
+        const int lane = threadIdx.x & 63;
+        const int wave = first_lane_int(threadIdx.x >> 6);   // uniform within the wavefront
+        const int n = lane & 15, kq = lane >> 4;
+        const int po = wave / NBE, rb = wave % NBE;
+        const int b = s.b, g = s.g;
+        const int G = p.G;
+        const int L = ld_meta(p.ctx_lens, b);
+        const int Q = ld_meta(p.q_lens, b);
+        const int R = p.rows_per_unit;
+        const int32_t *pt = p.page_table + (size_t)b * p.max_pages;
+        const int seg_end_tok = min(L, s.j1 * kPage);
+        const int full_end = min(L - Q + 1, seg_end_tok);
+
+        State st;
+        {
+            const int r = rb * 16 + n;
+            const bool row_ok = r < R && r / G < Q;
+            const int i = row_ok ? r / G : 0;
+            const int hl = row_ok ? r % G : 0;
+            st.lim = min(row_ok ? L - Q + i + 1 : L, seg_end_tok);
+            const uint16_t *qr = p.q + (((size_t)b * p.Qmax + i) * p.Hq + (size_t)g * G + hl) * kD + 8 * kq;
+#pragma unroll
+            for (int ks = 0; ks < 4; ks++)
+                st.qf[ks] = row_ok ? ld16(qr + 32 * ks) : u32x4_t{0u, 0u, 0u, 0u};
+            st.m_ref = -INFINITY;
+            st.lacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int jj = 0; jj < 8; jj++)
+                st.acc[jj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+
+        const int ngroups = (s.j1 - s.j0 + PS - 1) / PS;
+        Ring ring;
+        static_for<0, kDepth>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            load_group(p, pt, g, s.j0, s.j1, k, wave, lane, ring.template at<k>());
+        });
+        // group 0 into stage 0
+        store_group(lds, wave, lane, ring.template at<0>());
+        load_group(p, pt, g, s.j0, s.j1, kDepth, wave, lane, ring.template at<0>());
+        lds_barrier();
+
+        for (int it0 = 0; it0 < ngroups; it0 += kDepth) {
+            static_for<0, kDepth>([&](auto kc) {
+                constexpr int k = decltype(kc)::value;
+                constexpr int nk = (k + 1) % kDepth;   // ring slot of group it + 1
+                const int it = it0 + k;
+                if (it < ngroups) {
+                    store_group(lds + ((it + 1) & 1) * STAGE, wave, lane, ring.template at<nk>());
+                    load_group(p, pt, g, s.j0, s.j1, it + 1 + kDepth, wave, lane, ring.template at<nk>());
+                    const int j = s.j0 + it * PS + po;
+                    if (j < s.j1)
+                        page_step(p, st, lds + (it & 1) * STAGE + po * kPageLds, j, full_end, seg_end_tok, lane);
+                    lds_barrier();
+                }
+            });
+        }
+
+        // merge the PS page groups of each row block through LDS
+        if constexpr (PS > 1) {
+            Rec *rec = reinterpret_cast<Rec *>(lds);
+            if (po > 0) {
+                Rec &m = rec[(po - 1) * NBE + rb];
+#pragma unroll
+                for (int jj = 0; jj < 8; jj++)
+#pragma unroll
+                    for (int i = 0; i < 4; i++)
+                        m.acc[jj][i][lane] = st.acc[jj][i];
+#pragma unroll
+                for (int i = 0; i < 4; i++)
+                    m.lacc[i][lane] = st.lacc[i];
+                if (kq == 0)
+                    m.m[n] = st.m_ref;
+            }
+            lds_barrier();
+            if (po == 0) {
+                float mrow[4], M[4];
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    mrow[i] = __shfl(st.m_ref, 4 * kq + i);
+                    M[i] = mrow[i];
+                }
+#pragma unroll
+                for (int q = 1; q < PS; q++) {
+                    const Rec &m = rec[(q - 1) * NBE + rb];
+#pragma unroll
+                    for (int i = 0; i < 4; i++)
+                        M[i] = fmaxf(M[i], m.m[4 * kq + i]);
+                }
+                float a0[4];
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    a0[i] = mrow[i] == -INFINITY ? 0.0f : fast_exp2(mrow[i] - M[i]);
+                    st.lacc[i] *= a0[i];
+#pragma unroll
+                    for (int jj = 0; jj < 8; jj++)
+                        st.acc[jj][i] *= a0[i];
+                }
+#pragma unroll
+                for (int q = 1; q < PS; q++) {
+                    const Rec &m = rec[(q - 1) * NBE + rb];
+#pragma unroll
+                    for (int i = 0; i < 4; i++) {
+                        const float mq = m.m[4 * kq + i];
+                        const float aq = mq == -INFINITY ? 0.0f : fast_exp2(mq - M[i]);
+                        st.lacc[i] += aq * m.lacc[i][lane];
+#pragma unroll
+                        for (int jj = 0; jj < 8; jj++)
+                            st.acc[jj][i] += aq * m.acc[jj][i][lane];
+                    }
+                }
+                write_out(p, st, M, s, slot_id, rb, lane);
+            }
+            lds_barrier();
+        } else {
+            float M[4];
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+                M[i] = __shfl(st.m_ref, 4 * kq + i);
+            write_out(p, st, M, s, slot_id, rb, lane);
+            lds_barrier();
+        }
+    }
+
+    // Rows 16 rb + 4 kq + i, dims 8 n .. 8 n + 7 of the merged state.
+    __device__ __forceinline__ static void write_out(const AttnParams &p, const State &st, const float (&M)[4],
+                                     const Segment &s, int slot_id, int rb, int lane) {
+        const int n = lane & 15, kq = lane >> 4;
+        const int G = p.G, R = p.rows_per_unit, Q = ld_meta(p.q_lens, s.b);
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            const int r = rb * 16 + 4 * kq + i;
+            const int di = r / G;
+            if (r >= R || di >= Q)
+                continue;
+            const float l = st.lacc[i];
+            const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+            if (s.whole) {
+                uint16_t *dst = p.out + (((size_t)s.b * p.Qmax + di) * p.Hq + (size_t)s.g * G + r % G) * kD + 8 * n;
+                *reinterpret_cast<uint4 *>(dst) =
+                    make_uint4(pack_bf16x2(st.acc[0][i] * inv, st.acc[1][i] * inv),
+                               pack_bf16x2(st.acc[2][i] * inv, st.acc[3][i] * inv),
+                               pack_bf16x2(st.acc[4][i] * inv, st.acc[5][i] * inv),
+                               pack_bf16x2(st.acc[6][i] * inv, st.acc[7][i] * inv));
+            } else {
+                const size_t row = (size_t)slot_id * R + r;
+                float *dst = p.ws_o + row * kD + 8 * n;
+                *reinterpret_cast<float4 *>(dst) = make_float4(st.acc[0][i] * inv, st.acc[1][i] * inv,
+                                                               st.acc[2][i] * inv, st.acc[3][i] * inv);
+                *reinterpret_cast<float4 *>(dst + 4) = make_float4(st.acc[4][i] * inv, st.acc[5][i] * inv,
+                                                                   st.acc[6][i] * inv, st.acc[7][i] * inv);
+                if (n == 0)
+                    p.ws_lse[row] = l > 0.0f ? M[i] + __log2f(l) : -INFINITY;
+            }
+        }
+    }
+};
+
+// LDS bytes a team of NBE row blocks needs beyond the sequence prefix.
+template <int NBE>
+constexpr int team_lds() {
+    constexpr int stages = 2 * Team<NBE>::STAGE;
+    constexpr int recs = (Team<NBE>::PS - 1) * NBE * (int)sizeof(typename Team<NBE>::Rec);
+    return stages > recs ? stages : recs;
+}
+
+template <int NBE>
+__global__ __launch_bounds__(256) void verify_team_kernel(AttnParams p) {
+    extern __shared__ int s_pre[];
+    page_prefix(p, s_pre);
+    char *lds = reinterpret_cast<char *>(s_pre) + (((p.B + 1) * 4 + 15) & ~15);
+    const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
+    const int w = blockIdx.x;
+    const int64_t begin = worker_begin(ptot, w, p.W);
+    const int64_t end = worker_begin(ptot, w + 1, p.W);
+    for (int64_t x = begin; x < end;) {
+        const Segment s = locate(p, s_pre, x, end);
+        Team<NBE>::segment(p, s, x == begin ? 2 * w : 2 * w + 1, lds);
+        x = s.next;
+    }
+}
+
+}  // namespace
+
+typedef void (*kernel_fn)(AttnParams);
+
+// Kernel and its LDS need (beyond the prefix) for R = G * Qmax rows, head_dim 128.
+kernel_fn verify_team_variant(int rows, int *lds_bytes, int *nbe) {
+    if (rows <= 16) {
+        *nbe = 1;
+        *lds_bytes = team_lds<1>();
+        return verify_team_kernel<1>;
+    }
+    if (rows <= 32) {
+        *nbe = 2;
+        *lds_bytes = team_lds<2>();
+        return verify_team_kernel<2>;
+    }
+    *nbe = 4;
+    *lds_bytes = team_lds<4>();
+    return verify_team_kernel<4>;
+}
+
+}  // namespace tsattn

@@ -59,12 +59,13 @@ def upload(wl: synth.Workload, values: str = "host", device: str = "cuda") -> Di
                 q_lens=i32(wl.q_lens), out=out, out_full=out_full)
 
 
-def run(wl: synth.Workload, t: Dict[str, object], num_workers: int = 0, workspace=None, events=None):
+def run(wl: synth.Workload, t: Dict[str, object], num_workers: int = 0, workspace=None, events=None,
+        variant: int = 0):
     from . import binding
     return binding.decode_attn(t["q"], t["k_pages"], t["v_pages"], t["page_table"], t["ctx_lens"],
                                t["q_lens"], t["out"], wl.scale, workspace=workspace,
                                max_ctx_len=max(1, wl.max_ctx_len), num_workers=num_workers,
-                               events=events)
+                               events=events, variant=variant)
 
 
 def out_as_f64(t: Dict[str, object]) -> np.ndarray:

@@ -57,6 +57,18 @@ def test_bad_shapes_rejected(kw):
     assert st == -2
 
 
+def test_variant_checks():
+    s = base_shape(max_q_len=4)
+    s.variant = 3
+    assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) == 0
+    s.variant = b.VARIANT_TEAM          # team kernel needs head_dim 128
+    assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) == 0
+    s.head_dim = 128
+    assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) > 0
+    s.variant = b.VARIANT_WAVE
+    assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) > 0
+
+
 def test_page_size_must_be_16():
     s = base_shape()
     s.page_size = 32

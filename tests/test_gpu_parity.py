@@ -39,17 +39,26 @@ def test_device_fill_matches_host_generator(dev):
         assert np.array_equal(got, want)
 
 
+def variants_for(wl):
+    """Kernel variants that apply to a workload (both verify kernels at d128)."""
+    if wl.Qmax > 1 and wl.D == 128:
+        return (1, 2)
+    return (0,)
+
+
 def run_case(dev, orc, wl, workers=(0,), values="host"):
     _, device = dev
     ref = oracle_out(orc, wl)
     t = device.upload(wl, values=values)
-    for w in workers:
-        say(f"case {wl.name} B={wl.B} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} Qmax={wl.Qmax} "
-            f"lens={list(wl.ctx_lens)[:8]} q={list(wl.q_lens)[:8]} workers={w}")
-        device.run(wl, t, num_workers=w)
-        got = device.out_as_f64(t)
-        assert_parity(got, ref, f"{wl.name}/w{w}")
-        canary_ok(t, wl)
+    for var in variants_for(wl):
+        for w in workers:
+            say(f"case {wl.name} B={wl.B} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} Qmax={wl.Qmax} "
+                f"lens={list(wl.ctx_lens)[:8]} q={list(wl.q_lens)[:8]} workers={w} variant={var}")
+            t["out_full"].fill_(device.CANARY)
+            device.run(wl, t, num_workers=w, variant=var)
+            got = device.out_as_f64(t)
+            assert_parity(got, ref, f"{wl.name}/w{w}/v{var}")
+            canary_ok(t, wl)
     return t, ref
 
 
@@ -86,11 +95,11 @@ def test_small_grid(dev, orc, case):
 
 def test_one_key_returns_value_row_bitwise(dev, orc):
     _, device = dev
-    for Qmax in (1, 2):
+    for Qmax, var in ((1, 0), (2, 1), (2, 2)):
         wl = synth.make_workload("onekey", seed=9, cfg=small_cfg(32, 8, 128), ctx_lens=[1, 1, 1],
                                  q_lens=[1, 1, 1], Qmax=Qmax)
         t = device.upload(wl)
-        device.run(wl, t)
+        device.run(wl, t, variant=var)
         out = t["out"].view(__import__("torch").int16).cpu().numpy().view(np.uint16)
         vp = wl.v_pages()
         for b in range(3):
@@ -101,14 +110,14 @@ def test_one_key_returns_value_row_bitwise(dev, orc):
 def test_constant_values_give_exactly_that_value(dev):
     import torch
     _, device = dev
-    for q in (1, 4, 16):
+    for q, var in ((1, 0), (4, 1), (4, 2), (16, 1), (16, 2)):
         wl = synth.make_workload("constv", seed=4, cfg=small_cfg(32, 8, 128), ctx_lens=[q + 40, 3000],
                                  q_lens=[q, q])
         t = device.upload(wl, values="device")
         t["v_pages"].fill_(1.0)
-        device.run(wl, t)
+        device.run(wl, t, variant=var)
         got = device.out_as_f64(t)
-        assert (got[:, :q] == 1.0).all(), q
+        assert (got[:, :q] == 1.0).all(), (q, var)
 
 
 def test_page_relabel_is_bitwise_invariant(dev):
@@ -170,9 +179,10 @@ def test_split_points_do_not_change_the_result(dev):
                              q_lens=[16, 16])
     t = device.upload(wl, values="device")
     outs = []
-    for w in (1, 2, 7, 0, 300):
-        device.run(wl, t, num_workers=w)
-        outs.append(device.out_as_f64(t))
+    for var in (1, 2):
+        for w in (1, 2, 7, 0, 300):
+            device.run(wl, t, num_workers=w, variant=var)
+            outs.append(device.out_as_f64(t))
     for o in outs[1:]:
         assert_parity(o, outs[0], "split")
 
@@ -191,14 +201,15 @@ def test_full_size_config(dev, orc, name):
     say(f"full {name}: B={wl.B} sum_ctx={int(wl.ctx_lens.sum())} max={wl.max_ctx_len} "
         f"KV={wl.kv_bytes() / 1e9:.2f} GB")
     t = device.upload(wl, values="device")
-    device.run(wl, t)
-    got = device.out_as_f64(t)
-    canary_ok(t, wl)
-    assert np.isfinite(got).all()
     seqs = sample_seqs(wl, FULL[name])
-    sub = wl.subset(seqs)
-    ref = oracle_out(orc, sub)
-    assert_parity(got[seqs], ref, f"{name} seqs {seqs}")
+    ref = oracle_out(orc, wl.subset(seqs))
+    for var in variants_for(wl):
+        t["out_full"].fill_(device.CANARY)
+        device.run(wl, t, variant=var)      # variant 0 / auto is the benchmarked launch
+        got = device.out_as_f64(t)
+        canary_ok(t, wl)
+        assert np.isfinite(got).all()
+        assert_parity(got[seqs], ref, f"{name} seqs {seqs} variant {var}")
 
 
 SWEEP_CASES = [(b, 0) for b in synth.SWEEP_BATCHES] + \
