@@ -149,6 +149,9 @@ def main():
     ap.add_argument("--no-tail", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--only", choices=list(WORKLOADS), help="time one workload only (profiling)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="with --only: first copy BYTES with the library's plain copy kernel, "
+                         "so hardware byte counters can be scaled against a known transfer")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the attention path has no cross-GPU step; "
@@ -161,6 +164,13 @@ def main():
     torch.cuda.set_device(0)
 
     if args.only:
+        if args.calibrate_copy:
+            n = args.calibrate_copy // 16 * 16
+            src = torch.empty(n, dtype=torch.uint8, device="cuda")
+            dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+            binding.copy_bytes(dst, src)
+            torch.cuda.synchronize()
+            del src, dst
         r = time_workload(args.only, args.steps, args.warmup)
         r.pop("wl")
         print(json.dumps(r), flush=True)

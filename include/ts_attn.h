@@ -198,6 +198,12 @@ int ts_synth_page_table(int32_t batch, const int32_t *ctx_lens, int32_t page_siz
  * transfer. */
 int ts_copy_bytes(void *dst, const void *src, size_t bytes, void *stream);
 
+/* Plain streaming read of `bytes` (multiple of 16, 16-byte aligned): every
+ * word is loaded once by a grid of 2,048 blocks of 256 threads, and one fold
+ * per thread is written to `sink` (at least 2 MiB).  Its bandwidth is the
+ * practical HBM read ceiling the attention kernels are compared with. */
+int ts_stream_read(const void *src, size_t bytes, void *sink, size_t sink_bytes, void *stream);
+
 int ts_event_create(void **ev);
 int ts_event_destroy(void *ev);
 int ts_event_record(void *ev, void *stream);

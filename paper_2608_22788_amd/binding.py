@@ -54,7 +54,7 @@ class SweepPoint(ctypes.Structure):
 
 EXPORTS = ["ts_decode_attn_workspace_size", "ts_decode_attn", "ts_decode_attn_events",
            "ts_concurrency_sweep", "ts_synth_fill_bf16", "ts_synth_sweep_lengths",
-           "ts_synth_page_table", "ts_copy_bytes", "ts_event_create", "ts_event_destroy",
+           "ts_synth_page_table", "ts_copy_bytes", "ts_stream_read", "ts_event_create", "ts_event_destroy",
            "ts_event_record", "ts_event_elapsed_ms", "ts_status_string", "ts_last_error",
            "ts_version"]
 
@@ -90,6 +90,8 @@ def _load() -> ctypes.CDLL:
     lib.ts_synth_page_table.restype = ctypes.c_int
     lib.ts_copy_bytes.argtypes = [P, P, SZ, P]
     lib.ts_copy_bytes.restype = ctypes.c_int
+    lib.ts_stream_read.argtypes = [P, SZ, P, SZ, P]
+    lib.ts_stream_read.restype = ctypes.c_int
     lib.ts_event_create.argtypes = [ctypes.POINTER(P)]
     lib.ts_event_create.restype = ctypes.c_int
     lib.ts_event_destroy.argtypes = [P]
@@ -212,6 +214,13 @@ def page_table(ctx_lens: Sequence[int], max_pages_per_seq: int, seed: int) -> np
 def copy_bytes(dst, src, stream=None) -> None:
     n = src.numel() * src.element_size()
     check(lib.ts_copy_bytes(dst.data_ptr(), src.data_ptr(), n, _stream_ptr(stream)), "ts_copy_bytes")
+
+
+def stream_read(src, sink, stream=None) -> None:
+    """Read every byte of `src` once (HBM read-ceiling probe); `sink` >= 2 MiB."""
+    n = src.numel() * src.element_size()
+    check(lib.ts_stream_read(src.data_ptr(), n, sink.data_ptr(), sink.numel() * sink.element_size(),
+                             _stream_ptr(stream)), "ts_stream_read")
 
 
 class Event:

@@ -76,15 +76,16 @@ struct Plan {
 };
 
 // Number of workers sharing the KV stream.  MI355X has 256 compute units.
-// Measured on the bulk, MTP and block-draft workloads: the decode kernel is
-// best with 4 single-wavefront workers per unit (1024 in all; 2048 and 4096
-// are within 3 %), the team verify kernel with 1 (one row block) or 2
-// workgroups per unit.  Fewer workers also mean fewer split partials to merge.
+// Measured on the bulk, MTP and block-draft workloads: the decode kernel and
+// the single-wavefront verify kernel with one row block are best with 4
+// workers per unit (1024 in all; 2048 is within 3 %), the team verify kernel
+// with 1 (one row block) or 2 workgroups per unit.  Fewer workers also mean
+// fewer split partials to merge.
 // Small shapes get fewer workers so that each has at least a few pages.
 static int auto_workers(const ts_attn_shape *s, bool q1, bool team, int NB) {
     // Team kernels with one row block run one workgroup per compute unit (their
     // register use allows one wavefront per SIMD); with 2 or 4 row blocks, two.
-    int per_cu = q1 ? 4 : team ? (NB == 1 ? 1 : 2) : (NB <= 2 ? 8 : 4);
+    int per_cu = q1 ? 4 : team ? (NB == 1 ? 1 : 2) : (NB <= 1 ? 4 : NB <= 2 ? 8 : 4);
     int64_t w = 256LL * per_cu;
     const int64_t pages_ub = (int64_t)s->num_seqs * s->num_kv_heads *
                              ((s->max_ctx_len + kPage - 1) / kPage);
@@ -131,7 +132,10 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
     pl->q1 = (s->max_q_len == 1) && (G == 1 || G == 2 || G == 4 || G == 8);
     pl->rows_per_unit = G * s->max_q_len;
     pl->NB = (pl->rows_per_unit + 15) / 16;
-    pl->team = !pl->q1 && s->head_dim == 128 && s->variant != TS_VARIANT_WAVE;
+    // One row block fits one wavefront's registers and runs best that way
+    // (measured on the MTP workload); more row blocks need the team kernel.
+    pl->team = !pl->q1 && s->head_dim == 128 &&
+               (s->variant == TS_VARIANT_TEAM || (s->variant == TS_VARIANT_AUTO && pl->NB >= 2));
     pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team, pl->NB);
     const size_t slots = 2 * (size_t)pl->W;
     pl->ws_o_bytes = slots * pl->rows_per_unit * s->head_dim * sizeof(float);

@@ -28,22 +28,45 @@
 // data (even NaN) in unused slots never reaches the output.
 #include "attn_common.h"
 
+#include <type_traits>
+
 namespace tsattn {
 
 namespace {
 
 template <int NC>
 struct PageRegs {
-    uint4 k[2][NC];
-    uint4 v[2][NC];
+    u32x4_t k[2][NC];
+    u32x4_t v[2][NC];
 };
+
+// Calls f(std::integral_constant<int, I>) for I = B .. E - 1 (compile-time).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
 
 template <int D, int G>
 struct DecodeQ1 {
     static constexpr int NC = D / 64;   // 16-byte chunks per token row per lane
     static constexpr int NO = NC * 8;   // output dims per lane
+    static constexpr int kAhead = 2;    // pages in flight while one is computed
 
-    __device__ static void load_page(const AttnParams &p, const int32_t *pt, int j, int g,
+    struct Ring {
+        PageRegs<NC> r0, r1, r2;
+        template <int K>
+        __device__ __forceinline__ PageRegs<NC> &at() {
+            static_assert(K >= 0 && K < 3, "ring slot");
+            if constexpr (K == 0) return r0;
+            else if constexpr (K == 1) return r1;
+            else return r2;
+        }
+    };
+
+    __device__ __forceinline__ static void load_page(const AttnParams &p, const int32_t *pt, int j, int g,
                                      int slot, int part, PageRegs<NC> &r) {
         const int pid = ld_meta(pt, j);
         const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * D);
@@ -54,8 +77,94 @@ struct DecodeQ1 {
 #pragma unroll
             for (int c = 0; c < NC; c++) {
                 const int off = (slot + 8 * h) * D + 64 * c + 8 * part;
-                r.k[h][c] = *reinterpret_cast<const uint4 *>(kb + off);
-                r.v[h][c] = *reinterpret_cast<const uint4 *>(vb + off);
+                r.k[h][c] = ld_stream16(kb + off);
+                r.v[h][c] = ld_stream16(vb + off);
+            }
+        }
+    }
+
+    // One 16-token page: scores, online softmax, P.V for all G rows.
+    __device__ __forceinline__ static void page(const AttnParams &p, PageRegs<NC> &cur, int j, int L,
+                                                int slot, const uint32_t (&qv)[G][NC][4],
+                                                float (&o)[G][NO], float (&m_ref)[G], float (&lsum)[G]) {
+        // scores of the two tokens of this slot, all G rows
+        float x0[G], x1[G];
+#pragma unroll
+        for (int r = 0; r < G; r++) {
+            float a = 0.0f, c1 = 0.0f;
+#pragma unroll
+            for (int c = 0; c < NC; c++) {
+                a = dot2_bf16(cur.k[0][c].x, qv[r][c][0], a);
+                c1 = dot2_bf16(cur.k[1][c].x, qv[r][c][0], c1);
+                a = dot2_bf16(cur.k[0][c].y, qv[r][c][1], a);
+                c1 = dot2_bf16(cur.k[1][c].y, qv[r][c][1], c1);
+                a = dot2_bf16(cur.k[0][c].z, qv[r][c][2], a);
+                c1 = dot2_bf16(cur.k[1][c].z, qv[r][c][2], c1);
+                a = dot2_bf16(cur.k[0][c].w, qv[r][c][3], a);
+                c1 = dot2_bf16(cur.k[1][c].w, qv[r][c][3], c1);
+            }
+            x0[r] = sum8(a) * p.scale_log2;
+            x1[r] = sum8(c1) * p.scale_log2;
+        }
+
+        const bool tail = (j + 1) * kPage > L;       // wavefront-uniform
+        const int tok0 = j * kPage + slot;
+        const bool ok0 = !tail || tok0 < L;
+        const bool ok1 = !tail || tok0 + 8 < L;
+
+        bool need = false;
+        float mx[G];
+#pragma unroll
+        for (int r = 0; r < G; r++) {
+            mx[r] = fmaxf(ok0 ? x0[r] : -INFINITY, ok1 ? x1[r] : -INFINITY);
+            need |= mx[r] > m_ref[r] + kRescaleSlack;
+        }
+        if (__any(need)) {
+#pragma unroll
+            for (int r = 0; r < G; r++) {
+                const bool up = mx[r] > m_ref[r] + kRescaleSlack;
+                const float alpha = up ? fast_exp2(m_ref[r] - mx[r]) : 1.0f;
+                m_ref[r] = up ? mx[r] : m_ref[r];
+                lsum[r] *= alpha;
+#pragma unroll
+                for (int k = 0; k < NO; k++)
+                    o[r][k] *= alpha;
+            }
+        }
+
+        if (tail) {
+#pragma unroll
+            for (int c = 0; c < NC; c++) {
+                if (!ok0)
+                    cur.v[0][c] = u32x4_t{0u, 0u, 0u, 0u};
+                if (!ok1)
+                    cur.v[1][c] = u32x4_t{0u, 0u, 0u, 0u};
+            }
+        }
+
+        uint32_t pk[G];
+#pragma unroll
+        for (int r = 0; r < G; r++) {
+            const float p0 = ok0 ? fast_exp2(x0[r] - m_ref[r]) : 0.0f;
+            const float p1 = ok1 ? fast_exp2(x1[r] - m_ref[r]) : 0.0f;
+            pk[r] = pack_bf16x2(p0, p1);
+            lsum[r] = dot2_bf16(pk[r], 0x3F803F80u, lsum[r]);
+        }
+
+#pragma unroll
+        for (int c = 0; c < NC; c++) {
+            const uint32_t va[4] = {cur.v[0][c].x, cur.v[0][c].y, cur.v[0][c].z, cur.v[0][c].w};
+            const uint32_t vb[4] = {cur.v[1][c].x, cur.v[1][c].y, cur.v[1][c].z, cur.v[1][c].w};
+#pragma unroll
+            for (int w = 0; w < 4; w++) {
+                // (token slot, token slot + 8) pairs for dims 2w and 2w + 1
+                const uint32_t even = (va[w] & 0xffffu) | (vb[w] << 16);
+                const uint32_t odd = (va[w] >> 16) | (vb[w] & 0xffff0000u);
+#pragma unroll
+                for (int r = 0; r < G; r++) {
+                    o[r][8 * c + 2 * w] = dot2_bf16(even, pk[r], o[r][8 * c + 2 * w]);
+                    o[r][8 * c + 2 * w + 1] = dot2_bf16(odd, pk[r], o[r][8 * c + 2 * w + 1]);
+                }
             }
         }
     }
@@ -94,95 +203,26 @@ struct DecodeQ1 {
                 o[r][k] = 0.0f;
         }
 
-        // The prefetch of page j + 1 is issued unconditionally (the last page of
-        // the segment is simply loaded again at the end): a load under a branch
-        // would make the compiler wait for it before computing page j.
-        PageRegs<NC> cur, nxt;
-        load_page(p, pt, s.j0, g, slot, part, cur);
-        for (int j = s.j0; j < s.j1; j++) {
-            load_page(p, pt, min(j + 1, s.j1 - 1), g, slot, part, nxt);
-
-            // scores of the two tokens of this slot, all G rows
-            float x0[G], x1[G];
-#pragma unroll
-            for (int r = 0; r < G; r++) {
-                float a = 0.0f, c1 = 0.0f;
-#pragma unroll
-                for (int c = 0; c < NC; c++) {
-                    a = dot2_bf16(cur.k[0][c].x, qv[r][c][0], a);
-                    c1 = dot2_bf16(cur.k[1][c].x, qv[r][c][0], c1);
-                    a = dot2_bf16(cur.k[0][c].y, qv[r][c][1], a);
-                    c1 = dot2_bf16(cur.k[1][c].y, qv[r][c][1], c1);
-                    a = dot2_bf16(cur.k[0][c].z, qv[r][c][2], a);
-                    c1 = dot2_bf16(cur.k[1][c].z, qv[r][c][2], c1);
-                    a = dot2_bf16(cur.k[0][c].w, qv[r][c][3], a);
-                    c1 = dot2_bf16(cur.k[1][c].w, qv[r][c][3], c1);
+        // Pages are prefetched kAhead ahead into a ring of register sets
+        // addressed by compile-time index.  Every prefetch is issued
+        // unconditionally (past the segment the last page is loaded again): a
+        // load under a branch would make the compiler wait for it before the
+        // current page is computed.
+        Ring ring;
+        static_for<0, kAhead>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            load_page(p, pt, min(s.j0 + k, s.j1 - 1), g, slot, part, ring.template at<k>());
+        });
+        for (int j0 = s.j0; j0 < s.j1; j0 += kAhead + 1) {
+            static_for<0, kAhead + 1>([&](auto kc) {
+                constexpr int k = decltype(kc)::value;
+                const int j = j0 + k;
+                if (j < s.j1) {
+                    load_page(p, pt, min(j + kAhead, s.j1 - 1), g, slot, part,
+                              ring.template at<(k + kAhead) % (kAhead + 1)>());
+                    page(p, ring.template at<k>(), j, L, slot, qv, o, m_ref, lsum);
                 }
-                x0[r] = sum8(a) * p.scale_log2;
-                x1[r] = sum8(c1) * p.scale_log2;
-            }
-
-            const bool tail = (j + 1) * kPage > L;       // wavefront-uniform
-            const int tok0 = j * kPage + slot;
-            const bool ok0 = !tail || tok0 < L;
-            const bool ok1 = !tail || tok0 + 8 < L;
-
-            bool need = false;
-            float mx[G];
-#pragma unroll
-            for (int r = 0; r < G; r++) {
-                mx[r] = fmaxf(ok0 ? x0[r] : -INFINITY, ok1 ? x1[r] : -INFINITY);
-                need |= mx[r] > m_ref[r] + kRescaleSlack;
-            }
-            if (__any(need)) {
-#pragma unroll
-                for (int r = 0; r < G; r++) {
-                    const bool up = mx[r] > m_ref[r] + kRescaleSlack;
-                    const float alpha = up ? fast_exp2(m_ref[r] - mx[r]) : 1.0f;
-                    m_ref[r] = up ? mx[r] : m_ref[r];
-                    lsum[r] *= alpha;
-#pragma unroll
-                    for (int k = 0; k < NO; k++)
-                        o[r][k] *= alpha;
-                }
-            }
-
-            if (tail) {
-#pragma unroll
-                for (int c = 0; c < NC; c++) {
-                    if (!ok0)
-                        cur.v[0][c] = make_uint4(0, 0, 0, 0);
-                    if (!ok1)
-                        cur.v[1][c] = make_uint4(0, 0, 0, 0);
-                }
-            }
-
-            uint32_t pk[G];
-#pragma unroll
-            for (int r = 0; r < G; r++) {
-                const float p0 = ok0 ? fast_exp2(x0[r] - m_ref[r]) : 0.0f;
-                const float p1 = ok1 ? fast_exp2(x1[r] - m_ref[r]) : 0.0f;
-                pk[r] = pack_bf16x2(p0, p1);
-                lsum[r] = dot2_bf16(pk[r], 0x3F803F80u, lsum[r]);
-            }
-
-#pragma unroll
-            for (int c = 0; c < NC; c++) {
-                const uint32_t va[4] = {cur.v[0][c].x, cur.v[0][c].y, cur.v[0][c].z, cur.v[0][c].w};
-                const uint32_t vb[4] = {cur.v[1][c].x, cur.v[1][c].y, cur.v[1][c].z, cur.v[1][c].w};
-#pragma unroll
-                for (int w = 0; w < 4; w++) {
-                    // (token slot, token slot + 8) pairs for dims 2w and 2w + 1
-                    const uint32_t even = (va[w] & 0xffffu) | (vb[w] << 16);
-                    const uint32_t odd = (va[w] >> 16) | (vb[w] & 0xffff0000u);
-#pragma unroll
-                    for (int r = 0; r < G; r++) {
-                        o[r][8 * c + 2 * w] = dot2_bf16(even, pk[r], o[r][8 * c + 2 * w]);
-                        o[r][8 * c + 2 * w + 1] = dot2_bf16(odd, pk[r], o[r][8 * c + 2 * w + 1]);
-                    }
-                }
-            }
-            cur = nxt;
+            });
         }
 
         // merge the 8 token slots (lanes part, part + 8, ..., part + 56)

@@ -4,7 +4,9 @@
 // For a row with partials (o_s, lse_s), lse in log2 units:
 //   M = max_s lse_s,  w_s = 2^(lse_s - M),  out = sum_s w_s o_s / sum_s w_s,
 // and a split that saw no visible key (lse = -inf) has weight 0.  Partials
-// are visited in worker order, so the result is deterministic.
+// are visited in worker order, so the result is deterministic.  (The sums
+// are kept relative to the running maximum and rescaled when it grows, which
+// gives the same value up to rounding.)
 //
 // One wavefront handles 4 rows of one unit: lane (row, part) owns D/16
 // consecutive dims of one row.  The partial slots of a unit are found by
@@ -20,12 +22,28 @@ namespace {
 
 constexpr int kBatch = 8;   // partials in flight per lane
 
+// Slots of the workers wlo..whi that touched a unit starting at global page
+// us.  When every worker has at least one page (ptot >= W), worker w > wlo
+// began inside the unit (slot 2w) and only wlo needs its start compared with
+// us; otherwise workers with an empty range are skipped one by one.
 struct SlotWalk {
     int64_t ptot, us, wb;
     int w, whi, W;
+    bool dense;
+    __device__ SlotWalk(int64_t ptot_, int64_t us_, int wlo, int whi_, int W_)
+        : ptot(ptot_), us(us_), wb(worker_begin(ptot_, wlo, W_)), w(wlo), whi(whi_), W(W_),
+          dense(ptot_ >= W_) {}
     // Next up to kBatch slots; returns how many.
     __device__ int next(int *slots) {
         int n = 0;
+        if (dense) {
+            while (n < kBatch && w <= whi) {
+                slots[n++] = (wb >= us) ? 2 * w : 2 * w + 1;
+                wb = us;   // every later worker begins inside the unit
+                w++;
+            }
+            return n;
+        }
         while (n < kBatch && w <= whi) {
             const int64_t we = worker_begin(ptot, w + 1, W);
             if (we > wb)
@@ -65,54 +83,49 @@ __global__ __launch_bounds__(64) void merge_kernel(AttnParams p) {
     const bool row_ok = r < p.rows_per_unit && r / p.G < Q;
     const int rr = row_ok ? r : 0;   // keep addresses inside the workspace
 
-    // pass 1: the largest log-sum-exp of the row
-    float M = -INFINITY;
-    {
-        SlotWalk walk{ptot, us, worker_begin(ptot, wlo, p.W), wlo, whi, p.W};
-        int slots[kBatch];
-        for (int n; (n = walk.next(slots)) > 0;) {
-            float l[kBatch];
-#pragma unroll
-            for (int k = 0; k < kBatch; k++)
-                l[k] = k < n ? p.ws_lse[(size_t)slots[k] * p.rows_per_unit + rr] : -INFINITY;
-#pragma unroll
-            for (int k = 0; k < kBatch; k++)
-                M = fmaxf(M, l[k]);
-        }
-    }
-
-    // pass 2: weighted sum of the normalised partials
+    // One pass: each batch of partials is loaded at once; the running sums
+    // are rescaled to the batch's new maximum before the batch is added.
     float acc[VE];
 #pragma unroll
     for (int e = 0; e < VE; e++)
         acc[e] = 0.0f;
-    float den = 0.0f;
-    {
-        SlotWalk walk{ptot, us, worker_begin(ptot, wlo, p.W), wlo, whi, p.W};
-        int slots[kBatch];
-        for (int n; (n = walk.next(slots)) > 0;) {
-            float l[kBatch];
-            float4 v[kBatch][VE / 4];
+    float den = 0.0f, M = -INFINITY;
+    SlotWalk walk(ptot, us, wlo, whi, p.W);
+    int slots[kBatch];
+    for (int n; (n = walk.next(slots)) > 0;) {
+        float l[kBatch];
+        float4 v[kBatch][VE / 4];
 #pragma unroll
-            for (int k = 0; k < kBatch; k++) {
-                const size_t row = (size_t)(k < n ? slots[k] : slots[0]) * p.rows_per_unit + rr;
-                l[k] = k < n ? p.ws_lse[row] : -INFINITY;
-                const float *src = p.ws_o + row * D + VE * part;
+        for (int k = 0; k < kBatch; k++) {
+            const size_t row = (size_t)(k < n ? slots[k] : slots[0]) * p.rows_per_unit + rr;
+            l[k] = k < n ? p.ws_lse[row] : -INFINITY;
+            const float *src = p.ws_o + row * D + VE * part;
 #pragma unroll
-                for (int e = 0; e < VE / 4; e++)
-                    v[k][e] = *reinterpret_cast<const float4 *>(src + 4 * e);
-            }
+            for (int e = 0; e < VE / 4; e++)
+                v[k][e] = *reinterpret_cast<const float4 *>(src + 4 * e);
+        }
+        float Mb = M;
 #pragma unroll
-            for (int k = 0; k < kBatch; k++) {
-                const float wt = l[k] == -INFINITY ? 0.0f : fast_exp2(l[k] - M);
-                den += wt;
+        for (int k = 0; k < kBatch; k++)
+            Mb = fmaxf(Mb, l[k]);
+        if (Mb == -INFINITY)
+            continue;
+        const float a = M == -INFINITY ? 0.0f : fast_exp2(M - Mb);
+        den *= a;
 #pragma unroll
-                for (int e = 0; e < VE / 4; e++) {
-                    acc[4 * e + 0] += wt * v[k][e].x;
-                    acc[4 * e + 1] += wt * v[k][e].y;
-                    acc[4 * e + 2] += wt * v[k][e].z;
-                    acc[4 * e + 3] += wt * v[k][e].w;
-                }
+        for (int e = 0; e < VE; e++)
+            acc[e] *= a;
+        M = Mb;
+#pragma unroll
+        for (int k = 0; k < kBatch; k++) {
+            const float wt = l[k] == -INFINITY ? 0.0f : fast_exp2(l[k] - M);
+            den += wt;
+#pragma unroll
+            for (int e = 0; e < VE / 4; e++) {
+                acc[4 * e + 0] += wt * v[k][e].x;
+                acc[4 * e + 1] += wt * v[k][e].y;
+                acc[4 * e + 2] += wt * v[k][e].z;
+                acc[4 * e + 3] += wt * v[k][e].w;
             }
         }
     }

@@ -38,6 +38,7 @@ namespace {
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8_t, u); }
+__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t u) { return __builtin_bit_cast(bf16x8_t, u); }
 __device__ __forceinline__ s16x4_t as_s16x4(uint2 u) { return __builtin_bit_cast(s16x4_t, u); }
 
 template <int VE>
@@ -46,7 +47,7 @@ template <>
 struct VRow<8> {
     uint32_t w[4];
     __device__ void load(const uint16_t *p) {
-        uint4 t = *reinterpret_cast<const uint4 *>(p);
+        const u32x4_t t = ld_stream16(p);
         w[0] = t.x; w[1] = t.y; w[2] = t.z; w[3] = t.w;
     }
     __device__ void zero() { w[0] = w[1] = w[2] = w[3] = 0; }
@@ -55,7 +56,7 @@ template <>
 struct VRow<4> {
     uint32_t w[2];
     __device__ void load(const uint16_t *p) {
-        uint2 t = *reinterpret_cast<const uint2 *>(p);
+        const u32x2_t t = ld_stream8(p);
         w[0] = t.x; w[1] = t.y;
     }
     __device__ void zero() { w[0] = w[1] = 0; }
@@ -68,7 +69,7 @@ struct Verify {
     static constexpr int kRing = 2;   // pages in the register ring
 
     struct PageRegs {
-        uint4 k[KS];        // A operands of the score product
+        u32x4_t k[KS];      // A operands of the score product
         VRow<VE> v[4];      // value rows of the lane's 4 tokens
     };
 
@@ -79,7 +80,7 @@ struct Verify {
         const uint16_t *kb = p.k_pages + base + (size_t)n * D + 8 * kq;
 #pragma unroll
         for (int s = 0; s < KS; s++)
-            r.k[s] = *reinterpret_cast<const uint4 *>(kb + 32 * s);
+            r.k[s] = ld_stream16(kb + 32 * s);
         const uint16_t *vb = p.v_pages + base + (size_t)(4 * kq) * D + VE * n;
 #pragma unroll
         for (int i = 0; i < 4; i++)
@@ -132,12 +133,15 @@ struct Verify {
                 x[e] = sc[e] * p.scale_log2;
                 ok[e] = !masked || (t0 + 4 * kq + e < st.lim[rb]);
             }
+            // Lane-local check first: the row maximum (a cross-lane reduction over the
+            // four lanes of a row) is only needed when some score exceeds its row's
+            // reference by more than the slack, which is rare after the first page.
             float mx = fmaxf(fmaxf(ok[0] ? x[0] : -INFINITY, ok[1] ? x[1] : -INFINITY),
                              fmaxf(ok[2] ? x[2] : -INFINITY, ok[3] ? x[3] : -INFINITY));
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const bool up = mx > st.m_ref[rb] + kRescaleSlack;
-            if (__any(up)) {
+            if (__any(mx > st.m_ref[rb] + kRescaleSlack)) {
+                mx = fmaxf(mx, __shfl_xor(mx, 16));
+                mx = fmaxf(mx, __shfl_xor(mx, 32));
+                const bool up = mx > st.m_ref[rb] + kRescaleSlack;
                 const float alpha = up ? fast_exp2(st.m_ref[rb] - mx) : 1.0f;
                 st.m_ref[rb] = up ? mx : st.m_ref[rb];
 #pragma unroll

@@ -38,7 +38,6 @@ namespace tsattn {
 namespace {
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t u) { return __builtin_bit_cast(bf16x8_t, u); }
 __device__ __forceinline__ u32x4_t ld16(const void *p) { return *reinterpret_cast<const u32x4_t *>(p); }
@@ -73,21 +72,25 @@ struct Team {
     static constexpr int SLABS = 8 * PS;          // slabs per group
     static constexpr int PER_WAVE = SLABS / kTeam;  // slabs each wave loads per group
     static constexpr int STAGE = PS * kPageLds;   // LDS bytes per stage
-    static constexpr int kDepth = NBE == 1 ? 2 : 4;  // groups in flight in registers
+    static constexpr int kDepth = NBE == 1 ? 2 : NBE == 2 ? 4 : 8;  // groups in flight in registers
 
     struct Regs {
         u32x4_t s[PER_WAVE];
     };
     // kDepth register sets addressed only by compile-time index.
     struct Ring {
-        Regs r0, r1, r2, r3;
+        Regs r0, r1, r2, r3, r4, r5, r6, r7;
         template <int K>
         __device__ __forceinline__ Regs &at() {
-            static_assert(K >= 0 && K < 4, "ring slot");
+            static_assert(K >= 0 && K < 8, "ring slot");
             if constexpr (K == 0) return r0;
             else if constexpr (K == 1) return r1;
             else if constexpr (K == 2) return r2;
-            else return r3;
+            else if constexpr (K == 3) return r3;
+            else if constexpr (K == 4) return r4;
+            else if constexpr (K == 5) return r5;
+            else if constexpr (K == 6) return r6;
+            else return r7;
         }
     };
 
@@ -107,7 +110,7 @@ struct Team {
             const size_t off = sl < 4 ? (size_t)n * kD + 32 * sl + 8 * kq
                                       : (size_t)(4 * kq + sl - 4) * kD + 8 * n;
             const uint16_t *src = (sl < 4 ? p.k_pages : p.v_pages) + base + off;
-            r.s[t] = ld16(src);
+            r.s[t] = ld_stream16(src);
         }
     }
 
@@ -169,12 +172,15 @@ struct Team {
             x[e] = sc[e] * p.scale_log2;
             ok[e] = !masked || (t0 + 4 * kq + e < st.lim);
         }
+        // Lane-local check first: the row maximum (a cross-lane reduction over the
+        // four lanes of a row) is only needed when some score exceeds its row's
+        // reference by more than the slack, which is rare after the first page.
         float mx = fmaxf(fmaxf(ok[0] ? x[0] : -INFINITY, ok[1] ? x[1] : -INFINITY),
                          fmaxf(ok[2] ? x[2] : -INFINITY, ok[3] ? x[3] : -INFINITY));
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const bool up = mx > st.m_ref + kRescaleSlack;
-        if (__any(up)) {
+        if (__any(mx > st.m_ref + kRescaleSlack)) {
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const bool up = mx > st.m_ref + kRescaleSlack;
             const float alpha = up ? fast_exp2(st.m_ref - mx) : 1.0f;
             st.m_ref = up ? mx : st.m_ref;
 #pragma unroll

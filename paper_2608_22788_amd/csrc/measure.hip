@@ -15,6 +15,18 @@ __global__ __launch_bounds__(256) void copy_kernel(uint4 *dst, const uint4 *src,
         dst[i] = src[i];
 }
 
+// Reads every 16-byte word once and folds it into one word per thread, so the
+// loads cannot be dropped; the folds are written to `sink`.
+__global__ __launch_bounds__(256) void read_kernel(const uint4 *src, int64_t n, uint32_t *sink) {
+    uint32_t acc = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const uint4 v = src[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    sink[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = acc;
+}
+
 }  // namespace
 }  // namespace tsattn
 
@@ -42,6 +54,25 @@ int ts_copy_bytes(void *dst, const void *src, size_t bytes, void *stream) {
                        static_cast<const uint4 *>(src), n);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? TS_OK : hip_fail(e, "copy launch");
+}
+
+int ts_stream_read(const void *src, size_t bytes, void *sink, size_t sink_bytes, void *stream) {
+    clear_error();
+    if (!src || !sink)
+        return fail(TS_ERR_NULL, "NULL pointer");
+    if ((bytes & 15) || ((uintptr_t)src & 15))
+        return fail(TS_ERR_ARG, "stream read needs 16-byte sizes and alignment");
+    const int64_t blocks = 256 * 8;
+    if (sink_bytes < (size_t)blocks * 256 * sizeof(uint32_t))
+        return fail(TS_ERR_ARG, "sink needs %lld bytes", (long long)(blocks * 256 * 4));
+    int st = check_device();
+    if (st)
+        return st;
+    hipLaunchKernelGGL(read_kernel, dim3((unsigned)blocks), dim3(256), 0,
+                       reinterpret_cast<hipStream_t>(stream), static_cast<const uint4 *>(src),
+                       (int64_t)(bytes / 16), static_cast<uint32_t *>(sink));
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? TS_OK : hip_fail(e, "stream read launch");
 }
 
 int ts_event_create(void **ev) {
