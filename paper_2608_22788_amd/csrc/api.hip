@@ -78,14 +78,15 @@ struct Plan {
 // Number of workers sharing the KV stream.  MI355X has 256 compute units.
 // Measured on the bulk, MTP and block-draft workloads: the decode kernel and
 // the single-wavefront verify kernel with one row block are best with 4
-// workers per unit (1024 in all; 2048 is within 3 %), the team verify kernel
-// with 1 (one row block) or 2 workgroups per unit.  Fewer workers also mean
-// fewer split partials to merge.
+// workers per unit (1024 in all; 2048 is within 3 %); the team verify kernel
+// with 1 workgroup per unit for one row block and 4 (two resident at a time,
+// which evens out the finish times) for more.  Fewer workers also mean fewer
+// split partials to merge.
 // Small shapes get fewer workers so that each has at least a few pages.
 static int auto_workers(const ts_attn_shape *s, bool q1, bool team, int NB) {
     // Team kernels with one row block run one workgroup per compute unit (their
     // register use allows one wavefront per SIMD); with 2 or 4 row blocks, two.
-    int per_cu = q1 ? 4 : team ? (NB == 1 ? 1 : 2) : (NB <= 1 ? 4 : NB <= 2 ? 8 : 4);
+    int per_cu = q1 ? 4 : team ? (NB == 1 ? 1 : 4) : (NB <= 1 ? 4 : NB <= 2 ? 8 : 4);
     int64_t w = 256LL * per_cu;
     const int64_t pages_ub = (int64_t)s->num_seqs * s->num_kv_heads *
                              ((s->max_ctx_len + kPage - 1) / kPage);

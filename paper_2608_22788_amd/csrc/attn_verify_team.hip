@@ -9,22 +9,32 @@
 // split the rows of one page and with 16 rows they take four pages each.
 // A workgroup is one worker of the stream-K partition (attn_common.h).
 //
-// Staging.  A page is eight 1 KiB slabs: four K slabs (slab s holds, for
-// consumer lane l = 16 kq + n, key row n dims 32 s + 8 kq .. + 7: the A
-// operand of the score product) and four V slabs (slab i holds value row
-// 4 kq + i dims 8 n .. 8 n + 7).  Each lane loads the 16 bytes that the same
-// lane of every consumer wave will read, so global loads are coalesced row
-// segments and LDS reads are conflict-free consecutive 16-byte lanes.  The
-// four waves split the loading; loads run kDepth groups ahead in registers,
-// are written into one of two LDS stages, and one barrier per page group
+// Staging.  A page is loaded as eight 1 KiB slabs, one 16-byte piece per
+// lane: four K slabs (slab s holds, for consumer lane l = 16 kq + n, key row
+// n dims 32 s + 8 kq .. + 7: the A operand of the score product, stored in
+// lane order so reads are conflict-free consecutive 16 bytes) and four V
+// slabs (slab i: value row 4 kq + i, dims 8 n .. 8 n + 7), stored as the
+// page's 16 value rows in natural order with a 288-byte row pitch.  The four
+// waves split the loading; loads run kDepth groups ahead in registers, are
+// written into one of two LDS stages, and one barrier per page group
 // separates writing a stage from reading it.
 //
+// Value operand.  gfx950's LDS transpose read (ds_read_b64_tr_b16) hands lane
+// i' of each 16-lane group element i' % 4 of the 8-byte chunk addressed by
+// lane 4k + i' / 4 of that group, as element k.  So if lane (n, kq) addresses
+// value row 4 kq + n / 4, dims 16 jj + 4 (n % 4) .. + 3, every lane receives
+// rows 4 kq .. 4 kq + 3 of dim 16 jj + n: exactly the B operand of the j-th
+// P.V product, with no register shuffles.  With the 288-byte pitch the 16
+// lanes of a group touch 32 distinct banks.
+
 // Math per page and row block (l = lane, n = l % 16, kq = l / 16):
 //   S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (lane gets tokens 4kq..4kq+3 of
 //   row n); P = exp2(scale log2e S - m_ref) packed to bf16 in the same lane
-//   is the A operand of O += P V on v_mfma_f32_16x16x16_bf16; V rows are
-//   transposed in registers; row sums are P times a ones operand; m_ref is
-//   raised only when a score exceeds it by more than 8 (log2 units).
+//   is the A operand of O += P V on v_mfma_f32_16x16x16_bf16 (product jj
+//   covers dims 16 jj .. 16 jj + 15); row sums are P times a ones operand;
+//   m_ref is raised only when a score exceeds it by more than 8 (log2 units).
+//   Pages that need no mask (all but the last one or two of a sequence) take
+//   a path without any per-token selects.
 // At the end of a segment the PS waves of a row block merge their running
 // states through LDS with log-sum-exp weights; the first one writes.
 // Masks: key t is visible to draft row i iff t <= L - Q + i; keys past the
@@ -62,8 +72,10 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 constexpr int kD = 128;
-constexpr int kSlab = 1024;               // bytes per slab
-constexpr int kPageLds = 8 * kSlab;       // one page in fragment order
+constexpr int kSlab = 1024;               // bytes per K slab
+constexpr int kVPitch = 288;              // bytes per value row in LDS
+constexpr int kVOff = 4 * kSlab;          // value rows follow the K slabs
+constexpr int kPageLds = kVOff + kPage * kVPitch;   // one staged page
 constexpr int kTeam = 4;                  // wavefronts per workgroup
 
 template <int NBE>
@@ -72,7 +84,7 @@ struct Team {
     static constexpr int SLABS = 8 * PS;          // slabs per group
     static constexpr int PER_WAVE = SLABS / kTeam;  // slabs each wave loads per group
     static constexpr int STAGE = PS * kPageLds;   // LDS bytes per stage
-    static constexpr int kDepth = NBE == 1 ? 2 : NBE == 2 ? 4 : 8;  // groups in flight in registers
+    static constexpr int kDepth = NBE == 1 ? 2 : 4;  // groups in flight in registers
 
     struct Regs {
         u32x4_t s[PER_WAVE];
@@ -115,10 +127,14 @@ struct Team {
     }
 
     __device__ __forceinline__ static void store_group(char *stage, int wave, int lane, const Regs &r) {
+        const int n = lane & 15, kq = lane >> 4;
 #pragma unroll
         for (int t = 0; t < PER_WAVE; t++) {
             const int tau = wave + kTeam * t;
-            *reinterpret_cast<u32x4_t *>(stage + tau * kSlab + lane * 16) = r.s[t];
+            const int po = tau >> 3, sl = tau & 7;
+            char *pg = stage + po * kPageLds;
+            char *dst = sl < 4 ? pg + sl * kSlab + lane * 16 : pg + kVOff + (4 * kq + sl - 4) * kVPitch + 16 * n;
+            *reinterpret_cast<u32x4_t *>(dst) = r.s[t];
         }
     }
 
@@ -130,53 +146,52 @@ struct Team {
         float m_ref;
     };
 
+    // One page for this wave's row block.  `masked` (wavefront-uniform) is set
+    // only for the last page or two of a sequence; elsewhere no per-token
+    // select is executed.
     __device__ __forceinline__ static void page_step(const AttnParams &p, State &st, const char *pg, int j,
-                                     int full_end, int seg_end_tok, int lane) {
-        const int kq = lane >> 4;
-        u32x4_t kf[4], vr[4];
+                                                     bool masked, int seg_end_tok, int lane) {
+        const int n = lane & 15, kq = lane >> 4;
+        u32x4_t kf[4];
 #pragma unroll
         for (int s = 0; s < 4; s++)
             kf[s] = ld16(pg + s * kSlab + lane * 16);
+        // transpose-read address of this lane for product jj: + 32 jj bytes
+        typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
+        const char *vbase = pg + kVOff + (4 * kq + (n >> 2)) * kVPitch + 8 * (n & 3);
+        s16x4_t vt[8];
 #pragma unroll
-        for (int i = 0; i < 4; i++)
-            vr[i] = ld16(pg + (4 + i) * kSlab + lane * 16);
-        const int t0 = j * kPage;
-        const bool masked = t0 + kPage > full_end;            // wavefront-uniform
-        if (t0 + kPage > seg_end_tok) {
-#pragma unroll
-            for (int i = 0; i < 4; i++)
-                if (t0 + 4 * kq + i >= seg_end_tok)
-                    vr[i] = u32x4_t{0u, 0u, 0u, 0u};
-        }
-        // transpose: vt[jj] = dim 8 n + jj of tokens 4kq .. 4kq + 3
-        const uint32_t v0[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
-        const uint32_t v1[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
-        const uint32_t v2[4] = {vr[2].x, vr[2].y, vr[2].z, vr[2].w};
-        const uint32_t v3[4] = {vr[3].x, vr[3].y, vr[3].z, vr[3].w};
-        uint2 vt[8];
-#pragma unroll
-        for (int w = 0; w < 4; w++) {
-            vt[2 * w] = make_uint2((v0[w] & 0xffffu) | (v1[w] << 16), (v2[w] & 0xffffu) | (v3[w] << 16));
-            vt[2 * w + 1] = make_uint2((v0[w] >> 16) | (v1[w] & 0xffff0000u),
-                                       (v2[w] >> 16) | (v3[w] & 0xffff0000u));
-        }
+        for (int jj = 0; jj < 8; jj++)
+            vt[jj] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_s16x4 *)(__attribute__((address_space(3))) const char *)(vbase + 32 * jj));
 
         f32x4_t sc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < 4; s++)
             sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[s]), as_bf16x8(st.qf[s]), sc, 0, 0, 0);
         float x[4];
-        bool ok[4];
 #pragma unroll
-        for (int e = 0; e < 4; e++) {
+        for (int e = 0; e < 4; e++)
             x[e] = sc[e] * p.scale_log2;
-            ok[e] = !masked || (t0 + 4 * kq + e < st.lim);
+        const int t0 = j * kPage;
+        if (masked) {
+            // invisible keys score -inf; keys past the segment or context end
+            // also get zeroed value rows (stale data may be NaN, and 0 * NaN
+            // would poison the product)
+            s16x4_t keep;
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                keep[e] = (t0 + 4 * kq + e < seg_end_tok) ? (short)-1 : (short)0;
+                x[e] = (t0 + 4 * kq + e < st.lim) ? x[e] : -INFINITY;
+            }
+#pragma unroll
+            for (int jj = 0; jj < 8; jj++)
+                vt[jj] &= keep;
         }
         // Lane-local check first: the row maximum (a cross-lane reduction over the
         // four lanes of a row) is only needed when some score exceeds its row's
         // reference by more than the slack, which is rare after the first page.
-        float mx = fmaxf(fmaxf(ok[0] ? x[0] : -INFINITY, ok[1] ? x[1] : -INFINITY),
-                         fmaxf(ok[2] ? x[2] : -INFINITY, ok[3] ? x[3] : -INFINITY));
+        float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
         if (__any(mx > st.m_ref + kRescaleSlack)) {
             mx = fmaxf(mx, __shfl_xor(mx, 16));
             mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -192,16 +207,22 @@ struct Team {
                     st.acc[jj][i] *= ai;
             }
         }
-        const float p0 = ok[0] ? fast_exp2(x[0] - st.m_ref) : 0.0f;
-        const float p1 = ok[1] ? fast_exp2(x[1] - st.m_ref) : 0.0f;
-        const float p2 = ok[2] ? fast_exp2(x[2] - st.m_ref) : 0.0f;
-        const float p3 = ok[3] ? fast_exp2(x[3] - st.m_ref) : 0.0f;
-        const s16x4_t pa = as_s16x4(make_uint2(pack_bf16x2(p0, p1), pack_bf16x2(p2, p3)));
+        float pr[4];
+#pragma unroll
+        for (int e = 0; e < 4; e++)
+            pr[e] = fast_exp2(x[e] - st.m_ref);
+        if (masked) {
+            // a row with no visible key yet keeps m_ref = -inf: -inf - -inf
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                pr[e] = x[e] == -INFINITY ? 0.0f : pr[e];
+        }
+        const s16x4_t pa = as_s16x4(make_uint2(pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3])));
         const uint2 ones = make_uint2(0x3F803F80u, 0x3F803F80u);
         st.lacc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, as_s16x4(ones), st.lacc, 0, 0, 0);
 #pragma unroll
         for (int jj = 0; jj < 8; jj++)
-            st.acc[jj] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, as_s16x4(vt[jj]), st.acc[jj], 0, 0, 0);
+            st.acc[jj] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, vt[jj], st.acc[jj], 0, 0, 0);
     }
 
     // Per-wave merge record in LDS (for waves po > 0).
@@ -264,7 +285,8 @@ struct Team {
                     load_group(p, pt, g, s.j0, s.j1, it + 1 + kDepth, wave, lane, ring.template at<nk>());
                     const int j = s.j0 + it * PS + po;
                     if (j < s.j1)
-                        page_step(p, st, lds + (it & 1) * STAGE + po * kPageLds, j, full_end, seg_end_tok, lane);
+                        page_step(p, st, lds + (it & 1) * STAGE + po * kPageLds, j,
+                                  (j + 1) * kPage > full_end, seg_end_tok, lane);
                     lds_barrier();
                 }
             });
@@ -336,9 +358,9 @@ struct Team {
         }
     }
 
-    // Rows 16 rb + 4 kq + i, dims 8 n .. 8 n + 7 of the merged state.
+    // Rows 16 rb + 4 kq + i, dims 16 jj + n (jj = 0..7) of the merged state.
     __device__ __forceinline__ static void write_out(const AttnParams &p, const State &st, const float (&M)[4],
-                                     const Segment &s, int slot_id, int rb, int lane) {
+                                                     const Segment &s, int slot_id, int rb, int lane) {
         const int n = lane & 15, kq = lane >> 4;
         const int G = p.G, R = p.rows_per_unit, Q = ld_meta(p.q_lens, s.b);
 #pragma unroll
@@ -350,19 +372,16 @@ struct Team {
             const float l = st.lacc[i];
             const float inv = l > 0.0f ? 1.0f / l : 0.0f;
             if (s.whole) {
-                uint16_t *dst = p.out + (((size_t)s.b * p.Qmax + di) * p.Hq + (size_t)s.g * G + r % G) * kD + 8 * n;
-                *reinterpret_cast<uint4 *>(dst) =
-                    make_uint4(pack_bf16x2(st.acc[0][i] * inv, st.acc[1][i] * inv),
-                               pack_bf16x2(st.acc[2][i] * inv, st.acc[3][i] * inv),
-                               pack_bf16x2(st.acc[4][i] * inv, st.acc[5][i] * inv),
-                               pack_bf16x2(st.acc[6][i] * inv, st.acc[7][i] * inv));
+                uint16_t *dst = p.out + (((size_t)s.b * p.Qmax + di) * p.Hq + (size_t)s.g * G + r % G) * kD + n;
+#pragma unroll
+                for (int jj = 0; jj < 8; jj++)
+                    dst[16 * jj] = to_bf16(st.acc[jj][i] * inv);
             } else {
                 const size_t row = (size_t)slot_id * R + r;
-                float *dst = p.ws_o + row * kD + 8 * n;
-                *reinterpret_cast<float4 *>(dst) = make_float4(st.acc[0][i] * inv, st.acc[1][i] * inv,
-                                                               st.acc[2][i] * inv, st.acc[3][i] * inv);
-                *reinterpret_cast<float4 *>(dst + 4) = make_float4(st.acc[4][i] * inv, st.acc[5][i] * inv,
-                                                                   st.acc[6][i] * inv, st.acc[7][i] * inv);
+                float *dst = p.ws_o + row * kD + n;
+#pragma unroll
+                for (int jj = 0; jj < 8; jj++)
+                    dst[16 * jj] = st.acc[jj][i] * inv;
                 if (n == 0)
                     p.ws_lse[row] = l > 0.0f ? M[i] + __log2f(l) : -INFINITY;
             }
