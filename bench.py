@@ -21,6 +21,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -30,8 +31,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_GBPS = 8000.0          # MI355X HBM3E
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = ["attn_common.h", "attn_decode.hip", "attn_verify.hip", "attn_merge.hip", "api.hip"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.md")
+# Sources whose kernel a traffic figure was measured on, per workload.
+TRAFFIC_SOURCES = {"bulk": ["attn_common.h", "attn_decode.hip"]}
 
 WORKLOADS = {
     "bulk": "bulk pool decode: 256 seqs, q_len 1, 32 q / 8 kv heads, d128, page 16, "
@@ -46,26 +48,26 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_hash() -> str:
+def kernel_hash(name: str) -> str:
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in TRAFFIC_SOURCES.get(name, []):
         with open(os.path.join(ROOT, "paper_2608_22788_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
 def measured_traffic(name: str):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if they
-    were taken on the current kernel sources."""
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    they were taken on the current kernel sources (else None)."""
     try:
         with open(TRAFFIC_FILE) as f:
-            data = json.load(f)
-    except (OSError, ValueError):
+            text = f.read()
+    except OSError:
         return None
-    rec = data.get(name)
-    if not rec or rec.get("kernel_hash") != kernel_hash():
+    m = re.search(rf"^traffic {name} kernel_hash=(\w+) bytes_per_launch=(\d+)$", text, re.M)
+    if not m or m.group(1) != kernel_hash(name):
         return None
-    return rec.get("bytes_per_launch")
+    return int(m.group(2))
 
 
 def make_pools(wl, n_pools):

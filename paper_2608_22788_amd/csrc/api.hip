@@ -235,7 +235,7 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
         return hip_fail(e, "hipEventRecord");
     const int ngroups = (pl.rows_per_unit + 3) / 4;
     const unsigned merge_blocks = (unsigned)(p.B * p.Hkv * ngroups);
-    hipLaunchKernelGGL(merge_k, dim3(merge_blocks), dim3(kWave), lds, hs, p);
+    hipLaunchKernelGGL(merge_k, dim3(merge_blocks), dim3(4 * kWave), lds, hs, p);
     if ((e = hipGetLastError()) != hipSuccess)
         return hip_fail(e, "merge kernel launch");
     return TS_OK;
