@@ -4,9 +4,11 @@
 // Rows.  The G query heads of a KV group times the Qmax draft rows form
 // R = G * Qmax rows per (sequence, KV head) unit, in NBE blocks of 16
 // (NBE = 1, 2 or 4; R padded up).  Row r is draft position r / G of query
-// head g * G + r % G.  Wave w owns row block w % NBE of page w / NBE of each
-// group of PS = 4 / NBE consecutive pages, so with 64 rows the four waves
-// split the rows of one page and with 16 rows they take four pages each.
+// head g * G + r % G.  A group is PS * PPW consecutive pages, PS = 4 / NBE;
+// wave w owns row block w % NBE of pages (w / NBE) * PPW + 0 .. PPW - 1 of
+// it.  With 64 rows the four waves split the rows of two pages (two
+// independent chains per wave and barrier), with 16 rows they take a page
+// each.
 // A workgroup is one worker of the stream-K partition (attn_common.h).
 //
 // Staging.  A page is loaded as eight 1 KiB slabs, one 16-byte piece per
@@ -80,11 +82,13 @@ constexpr int kTeam = 4;                  // wavefronts per workgroup
 
 template <int NBE>
 struct Team {
-    static constexpr int PS = kTeam / NBE;        // pages per group
-    static constexpr int SLABS = 8 * PS;          // slabs per group
+    static constexpr int PS = kTeam / NBE;        // page splits across the waves
+    static constexpr int PPW = NBE == 4 ? 2 : 1;  // pages per wave per group
+    static constexpr int GP = PS * PPW;           // pages per group
+    static constexpr int SLABS = 8 * GP;          // slabs per group
     static constexpr int PER_WAVE = SLABS / kTeam;  // slabs each wave loads per group
-    static constexpr int STAGE = PS * kPageLds;   // LDS bytes per stage
-    static constexpr int kDepth = NBE == 1 ? 2 : 4;  // groups in flight in registers
+    static constexpr int STAGE = GP * kPageLds;   // LDS bytes per stage
+    static constexpr int kDepth = NBE == 2 ? 4 : 2;  // groups in flight in registers
 
     struct Regs {
         u32x4_t s[PER_WAVE];
@@ -106,7 +110,7 @@ struct Team {
         }
     };
 
-    // Issue this wave's loads of group `grp` (pages j0 + grp * PS + po).  Pages
+    // Issue this wave's loads of group `grp` (pages j0 + grp * GP + q).  Pages
     // past the segment are clamped to its last page rather than skipped: a load
     // under a branch would make the compiler wait for it at the join.
     __device__ __forceinline__ static void load_group(const AttnParams &p, const int32_t *pt, int g, int j0, int j1,
@@ -116,7 +120,7 @@ struct Team {
         for (int t = 0; t < PER_WAVE; t++) {
             const int tau = wave + kTeam * t;
             const int po = tau >> 3, sl = tau & 7;
-            const int j = min(j0 + grp * PS + po, j1 - 1);
+            const int j = min(j0 + grp * GP + po, j1 - 1);
             const int pid = ld_meta(pt, j);
             const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * kD);
             const size_t off = sl < 4 ? (size_t)n * kD + 32 * sl + 8 * kq
@@ -264,7 +268,7 @@ struct Team {
                 st.acc[jj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
 
-        const int ngroups = (s.j1 - s.j0 + PS - 1) / PS;
+        const int ngroups = (s.j1 - s.j0 + GP - 1) / GP;
         Ring ring;
         static_for<0, kDepth>([&](auto kc) {
             constexpr int k = decltype(kc)::value;
@@ -283,10 +287,14 @@ struct Team {
                 if (it < ngroups) {
                     store_group(lds + ((it + 1) & 1) * STAGE, wave, lane, ring.template at<nk>());
                     load_group(p, pt, g, s.j0, s.j1, it + 1 + kDepth, wave, lane, ring.template at<nk>());
-                    const int j = s.j0 + it * PS + po;
-                    if (j < s.j1)
-                        page_step(p, st, lds + (it & 1) * STAGE + po * kPageLds, j,
-                                  (j + 1) * kPage > full_end, seg_end_tok, lane);
+#pragma unroll
+                    for (int pp = 0; pp < PPW; pp++) {
+                        const int q = po * PPW + pp;          // page within the group
+                        const int j = s.j0 + it * GP + q;
+                        if (j < s.j1)
+                            page_step(p, st, lds + (it & 1) * STAGE + q * kPageLds, j,
+                                      (j + 1) * kPage > full_end, seg_end_tok, lane);
+                    }
                     lds_barrier();
                 }
             });
