@@ -28,8 +28,14 @@ def hipcc() -> str:
 
 
 def flags(extra=()):
+    # -amdgpu-mfma-vgpr-form keeps matrix-core accumulators in ordinary VGPRs.
+    # Otherwise they are placed in AGPRs, and because the online softmax
+    # rescales them with VALU ops on a (rarely taken) branch, the compiler
+    # copied every accumulator AGPR -> VGPR -> AGPR on every page: 72 of the
+    # 83 VALU instructions per page in the block-draft verify kernel.
     return [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            "-mllvm", "-amdgpu-mfma-vgpr-form",
             "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}", *extra]
 
 

@@ -71,29 +71,62 @@ int check_device() {
 struct Plan {
     bool q1;          // one-token VALU kernel, else a matrix-core verify kernel
     bool team;        // verify by four-wavefront teams sharing pages in LDS (head_dim 128)
+    bool auto_w;      // worker count chosen by the library (W is then an upper bound)
     int G, NB, rows_per_unit, W;
     size_t ws_o_bytes, ws_lse_off, ws_bytes;
 };
 
 // Number of workers sharing the KV stream.  MI355X has 256 compute units.
-// Measured on the bulk, MTP and block-draft workloads: the decode kernel and
-// the single-wavefront verify kernel with one row block are best with 4
-// workers per unit (1024 in all; 2048 is within 3 %); the team verify kernel
-// with 1 workgroup per unit for one row block and 4 (two resident at a time,
-// which evens out the finish times) for more.  Fewer workers also mean fewer
-// split partials to merge.
-// Small shapes get fewer workers so that each has at least a few pages.
+// Measured on the bulk, MTP and block-draft workloads, the best count is one
+// full round of resident workers: all of them start together and finish
+// together, where a partial second round leaves most of the chip idle at the
+// end.  The table below is the measured residency per compute unit (it also
+// bounds the workspace); at launch the auto count is further capped by the
+// occupancy the HIP runtime reports for the compiled kernel.
+static int per_cu_bound(bool q1, bool team, int NB) {
+    if (q1)
+        return 4;              // decode: 4 single-wavefront workers
+    if (team)
+        return NB >= 3 ? 3 : 2;   // 64 rows: 3 teams (166 VGPRs); 16-32 rows: 2
+    return 4;                  // single-wavefront verify
+}
+
 static int auto_workers(const ts_attn_shape *s, bool q1, bool team, int NB) {
-    // Team kernels with one row block run one workgroup per compute unit (their
-    // register use allows one wavefront per SIMD); with 2 or 4 row blocks, two.
-    int per_cu = q1 ? 4 : team ? (NB == 1 ? 1 : 4) : (NB <= 1 ? 4 : NB <= 2 ? 8 : 4);
-    int64_t w = 256LL * per_cu;
+    int64_t w = 256LL * per_cu_bound(q1, team, NB);
+    // Small shapes get fewer workers so that each has at least a few pages.
     const int64_t pages_ub = (int64_t)s->num_seqs * s->num_kv_heads *
                              ((s->max_ctx_len + kPage - 1) / kPage);
     const int64_t by_size = (pages_ub + 7) / 8;
     if (by_size < w)
         w = by_size;
     return (int)(w < 1 ? 1 : w);
+}
+
+// Workgroups of `k` resident per compute unit times the compute units, or 0
+// if the runtime cannot tell.  Cached per kernel and device.
+static int resident_workers(kernel_fn k, int threads, size_t lds) {
+    static std::mutex mu;
+    struct Entry { kernel_fn k; int dev; int threads; size_t lds; int n; };
+    static Entry cache[64];
+    static int ncache = 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return 0;
+    std::lock_guard<std::mutex> lock(mu);
+    for (int i = 0; i < ncache; i++)
+        if (cache[i].k == k && cache[i].dev == dev && cache[i].threads == threads && cache[i].lds == lds)
+            return cache[i].n;
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k), threads, lds) !=
+            hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    const int n = per_cu * cus;
+    if (ncache < 64)
+        cache[ncache++] = Entry{k, dev, threads, lds, n};
+    return n;
 }
 
 int make_plan(const ts_attn_shape *s, Plan *pl) {
@@ -137,6 +170,7 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
     // (measured on the MTP workload); more row blocks need the team kernel.
     pl->team = !pl->q1 && s->head_dim == 128 &&
                (s->variant == TS_VARIANT_TEAM || (s->variant == TS_VARIANT_AUTO && pl->NB >= 2));
+    pl->auto_w = s->num_workers == 0;
     pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team, pl->NB);
     const size_t slots = 2 * (size_t)pl->W;
     pl->ws_o_bytes = slots * pl->rows_per_unit * s->head_dim * sizeof(float);
@@ -224,6 +258,13 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
     if (!main_k || !merge_k)
         return fail(TS_ERR_UNSUPPORTED, "no kernel for head_dim %d, G %d, rows %d", p.D, pl.G,
                     pl.rows_per_unit);
+    if (pl.auto_w) {
+        // one full round of resident workers (the workspace is sized for pl.W)
+        const int resident = resident_workers(main_k, main_threads, main_lds);
+        if (resident > 0 && resident < pl.W)
+            pl.W = resident;
+        p.W = pl.W;
+    }
 
     hipError_t e;
     if (ev_begin && (e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_begin), hs)) != hipSuccess)
