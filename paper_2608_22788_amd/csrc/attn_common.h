@@ -127,31 +127,48 @@ __device__ __forceinline__ int seq_pages(const AttnParams &p, int b) {
 
 // Exclusive prefix of seq_pages into s_pre[0..B] (s_pre[B] = total), computed
 // by the first wavefront of the block; every thread must call it (it ends in
-// a block barrier).  Lane t scans a contiguous run of sequences.
+// a block barrier).  Sequences are taken in batches of 64 * kPrefixRun: lane t
+// owns the run of kPrefixRun consecutive sequences starting at t * kPrefixRun.
+// All lengths of a batch are loaded before any is used (one memory latency
+// for up to 512 sequences), the run totals are scanned across the wavefront
+// once, and each lane then writes its run's prefixes.
+constexpr int kPrefixRun = 8;
+
 __device__ inline void page_prefix(const AttnParams &p, int *s_pre) {
     if (threadIdx.x < kWave) {
         const int lane = threadIdx.x;
-        const int per = (p.B + kWave - 1) / kWave;
-        const int lo = lane * per;
-        const int hi = min(lo + per, p.B);
-        int run = 0;
-        for (int b = lo; b < hi; b++)
-            run += seq_pages(p, b);
-        // inclusive scan of the run totals across the wavefront
-        int incl = run;
+        int base = 0;
+        for (int b0 = 0; b0 < p.B; b0 += kPrefixRun * kWave) {
+            const int first = b0 + lane * kPrefixRun;
+            int n[kPrefixRun];
+            int run = 0;
 #pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-            int y = __shfl_up(incl, off, kWave);
-            if (lane >= off)
-                incl += y;
+            for (int k = 0; k < kPrefixRun; k++) {
+                // unconditional load at a clamped index, so that every load
+                // is issued before the first wait
+                const int b = first + k;
+                const int v = seq_pages(p, min(b, p.B - 1));
+                n[k] = b < p.B ? v : 0;
+                run += n[k];
+            }
+            int incl = run;
+#pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                const int y = __shfl_up(incl, off, kWave);
+                if (lane >= off)
+                    incl += y;
+            }
+            int acc = base + incl - run;
+#pragma unroll
+            for (int k = 0; k < kPrefixRun; k++) {
+                if (first + k < p.B)
+                    s_pre[first + k] = acc;
+                acc += n[k];
+            }
+            base += __shfl(incl, kWave - 1, kWave);
         }
-        int acc = incl - run;
-        for (int b = lo; b < hi; b++) {
-            s_pre[b] = acc;
-            acc += seq_pages(p, b);
-        }
-        if (lane == kWave - 1)
-            s_pre[p.B] = incl;
+        if (lane == 0)
+            s_pre[p.B] = base;
     }
     __syncthreads();
 }

@@ -93,6 +93,21 @@ def test_small_grid(dev, orc, case):
     run_case(dev, orc, wl, workers=(0, 1, 3, 40))
 
 
+@pytest.mark.parametrize("B,Qmax", [(513, 1), (1100, 4), (4096, 1)])
+def test_many_sequences(dev, orc, B, Qmax):
+    """Past the 512 sequences whose lengths the partition loads in one batch,
+    up to the largest supported batch (4096), with ragged lengths and some
+    sequences skipped (q_len 0)."""
+    rng = np.random.default_rng(B)
+    ctx = rng.integers(1, 90, size=B)
+    ctx[rng.integers(0, B, size=8)] = 700
+    q = np.minimum(rng.integers(0, Qmax + 1, size=B) if Qmax > 1 else np.ones(B, np.int64), ctx)
+    q[rng.integers(0, B, size=5)] = 0
+    wl = synth.make_workload(f"many{B}", seed=B, cfg=small_cfg(8, 2, 64), ctx_lens=ctx.tolist(),
+                             q_lens=q.tolist(), Qmax=Qmax, poison=True, spare_pages=1)
+    run_case(dev, orc, wl, workers=(0, 5, 2000))
+
+
 def test_one_key_returns_value_row_bitwise(dev, orc):
     _, device = dev
     for Qmax, var in ((1, 0), (2, 1), (2, 2)):
