@@ -13,7 +13,8 @@ in a row.
 Printed: one JSON line with the bulk KV GB/s as ``value``, the roofline of
 the streaming kernel (its average duration from HIP events recorded around
 it on its own stream), the float64 oracle timed on this host's cores, the
-two tail-pool verify workloads and the concurrency curve (seed 0).
+two tail-pool verify workloads and the concurrency curve (mean, min and max
+over 5 seeds per batch size).
 """
 from __future__ import annotations
 
@@ -32,8 +33,15 @@ sys.path.insert(0, ROOT)
 
 PEAK_GBPS = 8000.0          # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.md")
-# Sources whose kernel a traffic figure was measured on, per workload.
-TRAFFIC_SOURCES = {"bulk": ["attn_common.h", "attn_decode.hip"]}
+# Files whose content decides the streaming kernel of each workload; a traffic
+# figure counts only while their hash matches the one it was measured on.
+TRAFFIC_SOURCES = {
+    "bulk": ["csrc/attn_common.h", "csrc/attn_decode.hip", "build.py"],
+    "mtp": ["csrc/attn_common.h", "csrc/attn_verify.hip", "build.py"],
+    "dflash": ["csrc/attn_common.h", "csrc/attn_verify_team.hip", "build.py"],
+}
+KERNELS = {"bulk": "decode_q1_kernel<128,4>", "mtp": "verify_kernel<128,1>",
+           "dflash": "verify_team_kernel<4>"}
 
 WORKLOADS = {
     "bulk": "bulk pool decode: 256 seqs, q_len 1, 32 q / 8 kv heads, d128, page 16, "
@@ -51,7 +59,7 @@ def log(*a):
 def kernel_hash(name: str) -> str:
     h = hashlib.sha256()
     for f in TRAFFIC_SOURCES.get(name, []):
-        with open(os.path.join(ROOT, "paper_2608_22788_amd", "csrc", f), "rb") as fh:
+        with open(os.path.join(ROOT, "paper_2608_22788_amd", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
@@ -97,7 +105,7 @@ def time_workload(name, steps, warmup, min_rotation=4 << 30):
         f"KV={kv / 1e9:.3f} GB pools={n_pools}")
     t, pools = make_pools(wl, n_pools)
     shape = binding.shape_of(t["q"], t["k_pages"], t["page_table"], wl.max_ctx_len)
-    ws = torch.empty(binding.workspace_size(shape), dtype=torch.uint8, device="cuda")
+    ws = binding.new_workspace(binding.workspace_size(shape))
     ev = [(binding.Event(), binding.Event()) for _ in range(steps)]
 
     def call(i, events=None):
@@ -125,21 +133,40 @@ def time_workload(name, steps, warmup, min_rotation=4 << 30):
                 tokens_per_s=qtok / (ms_step * 1e-3), n_pools=n_pools, wl=wl)
 
 
-def cpu_baseline(wl):
-    """The float64 oracle on this host's cores over the whole bulk call."""
+def cpu_baseline(wl, min_seconds=10.0, max_runs=50):
+    """The float64 oracle on this host's cores over the whole bulk call,
+    repeated until about min_seconds of work (bounded by max_runs)."""
     import oracle
-    from paper_2608_22788_amd import synth  # noqa: F401
     orc = oracle.load()
     log("[bench] cpu baseline: generating host inputs")
     q, k, v = wl.q_values(), wl.k_pages(), wl.v_pages()
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
     log(f"[bench] cpu baseline: oracle on {threads} threads")
-    t0 = time.perf_counter()
-    orc.attention(q, k, v, wl.page_table, wl.ctx_lens, wl.q_lens, wl.scale, nthreads=threads)
-    dt = time.perf_counter() - t0
+    runs, t0 = 0, time.perf_counter()
+    while runs < max_runs:
+        orc.attention(q, k, v, wl.page_table, wl.ctx_lens, wl.q_lens, wl.scale, nthreads=threads)
+        runs += 1
+        if time.perf_counter() - t0 >= min_seconds:
+            break
+    dt = (time.perf_counter() - t0) / runs
     return dict(value=wl.kv_bytes() / dt / 1e9, unit="GB/s", cores=threads, kind="oracle",
                 sample=f"whole bulk call ({wl.B} seqs, {int(wl.ctx_lens.sum())} context tokens), "
-                       f"float64, {dt:.2f} s")
+                       f"float64, {runs} runs, {dt:.3f} s each")
+
+
+def sweep_summary(points):
+    """Per batch size: mean, min and max over seeds of the sweep figures."""
+    out = []
+    for b in sorted({p["batch"] for p in points}):
+        ps = [p for p in points if p["batch"] == b]
+        row = dict(batch=b, q_len=ps[0]["q_len"], seeds=len(ps))
+        for f, nd in (("kv_gbps", 1), ("hbm_frac", 4), ("tokens_per_s", 0), ("tau_us", 2)):
+            xs = np.array([p[f] for p in ps])
+            row[f] = round(float(xs.mean()), nd)
+            row[f + "_min"] = round(float(xs.min()), nd)
+            row[f + "_max"] = round(float(xs.max()), nd)
+        out.append(row)
+    return out
 
 
 def main():
@@ -150,6 +177,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-tail", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--sweep-seeds", type=int, default=5)
     ap.add_argument("--only", choices=list(WORKLOADS), help="time one workload only (profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="with --only: first copy BYTES with the library's plain copy kernel, "
@@ -186,13 +214,13 @@ def main():
             r.pop("wl")
             tail[name] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
             tail[name]["hbm_frac"] = round(r["kv_gbps"] / PEAK_GBPS, 4)
+            tail[name]["kernel"] = KERNELS[name]
+            tail[name]["kernel_frac"] = round(r["kernel_gbps"] / PEAK_GBPS, 4)
+            tail[name]["traffic"] = measured_traffic(name)
     sweep = []
     if not args.no_sweep:
-        log("[bench] concurrency sweep (seed 0)")
-        for p in binding.concurrency_sweep(seeds=1, warmup=5, iters=30):
-            sweep.append(dict(batch=p["batch"], q_len=p["q_len"], kv_gbps=round(p["kv_gbps"], 1),
-                              hbm_frac=round(p["hbm_frac"], 4), tokens_per_s=round(p["tokens_per_s"]),
-                              tau_us=round(p["tau_us"], 2)))
+        log(f"[bench] concurrency sweep ({args.sweep_seeds} seeds)")
+        sweep = sweep_summary(binding.concurrency_sweep(seeds=args.sweep_seeds, warmup=5, iters=30))
     cpu = None if args.no_cpu_baseline else cpu_baseline(bulk["wl"])
 
     achieved = bulk["kernel_gbps"]
@@ -217,12 +245,12 @@ def main():
         "tokens_per_s": round(bulk["tokens_per_s"]),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_GBPS, 4), "traffic": traffic,
-                     "kernel": "decode_q1_kernel<128,4>",
+                     "kernel": KERNELS["bulk"],
                      "kernel_ms_mean": round(bulk["kernel_ms_mean"], 5),
                      "alg_bytes_per_launch": bulk["alg_bytes"]},
         "cpu_baseline": cpu,
         "tail": tail,
-        "sweep_seed0": sweep,
+        "sweep": sweep,
     }
     print(json.dumps(line), flush=True)
 

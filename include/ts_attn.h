@@ -35,16 +35,22 @@
  * library allocates nothing inside ts_decode_attn, never synchronises it and
  * never reads device data on the host, so a call can be captured into a HIP
  * graph.  Inputs are read-only; out is written only at rows i < q_lens[b]
- * (q_lens[b] = 0 skips sequence b); workspace contents are undefined on
- * return, and concurrent calls need distinct workspaces.  Every entry point
+ * (q_lens[b] = 0 skips sequence b).  The workspace starts with a fixed
+ * 1 MiB area of arrival counters (one per (sequence, KV head)), followed by
+ * split partial results.  It must be zero-filled before its first use (e.g.
+ * hipMemset once after allocation); every completed call leaves the counters
+ * zero again and never writes partial results over them, so a workspace can
+ * be reused by any later call, of any shape, on one stream.  Calls that may
+ * run concurrently need distinct workspaces.  Every entry point
  * returns TS_OK (0) or a negative ts_status; on error nothing is launched and
  * ts_last_error() describes the cause.  No C++ exception crosses the ABI.
  *
  * Device-side preconditions (1 <= q_lens[b] <= ctx_lens[b] <= max_ctx_len,
  * ctx_lens[b] <= max_pages_per_seq * page_size, q_lens[b] <= max_q_len, page
  * ids in [0, num_pages)) are the caller's to keep on the fast path; with the
- * environment variable TS_DEBUG=1 a checking kernel verifies them first, the
- * call synchronises and returns TS_ERR_SHAPE if any fails.
+ * environment variable TS_DEBUG=1 a checking kernel verifies them (and that
+ * the workspace counters are zero) first, the call synchronises and returns
+ * TS_ERR_SHAPE (TS_ERR_WORKSPACE for the counters) if any fails.
  */
 #ifndef TS_ATTN_H
 #define TS_ATTN_H
@@ -71,9 +77,9 @@ typedef enum ts_status {
 /* Host-known description of one call.  Supported: page_size 16; head_dim 64
  * or 128; num_q_heads a multiple of num_kv_heads with group size
  * G = num_q_heads / num_kv_heads in 1..16 and G * max_q_len <= 64;
- * max_q_len in 1..16; num_seqs >= 1.  max_ctx_len is an upper bound on
- * ctx_lens, used only for validation; the launch grid depends on the shape
- * alone.  num_workers = 0 lets the library choose how many workers (one
+ * max_q_len in 1..16; num_seqs in 1..4096; num_seqs * num_kv_heads <= 2^18.
+ * max_ctx_len is an upper bound on ctx_lens, used only for validation; the
+ * launch grid depends on the shape alone.  num_workers = 0 lets the library choose how many workers (one
  * wavefront, or a four-wavefront team for verify at head_dim 128) share the
  * KV stream; a positive value fixes it (the result does not depend on it
  * beyond rounding; tests use it to vary the split points).  variant selects
@@ -101,23 +107,24 @@ typedef struct ts_attn_shape {
 } ts_attn_shape;
 
 /* Bytes of device workspace ts_decode_attn needs for this shape (split-KV
- * partial outputs and their log-sum-exp).  Host only; returns 0 and sets
- * ts_last_error() for an unsupported shape. */
+ * partial outputs, their log-sum-exp and the per-unit arrival counters).
+ * Host only; returns 0 and sets ts_last_error() for an unsupported shape. */
 size_t ts_decode_attn_workspace_size(const ts_attn_shape *shape);
 
 /* Paged decode / verify attention as defined above, enqueued on `stream`
  * (a hipStream_t; NULL is the default stream).  `scale` multiplies the dot
  * products (typically 1/sqrt(head_dim)).  `workspace` is device memory of at
- * least ts_decode_attn_workspace_size(shape) bytes, 256-byte aligned. */
+ * least ts_decode_attn_workspace_size(shape) bytes, 256-byte aligned,
+ * zero-filled before its first use (see above). */
 int ts_decode_attn(const ts_attn_shape *shape, const void *q, const void *k_pages,
                    const void *v_pages, const int32_t *page_table, const int32_t *ctx_lens,
                    const int32_t *q_lens, void *out, float scale, void *workspace,
                    size_t workspace_bytes, void *stream);
 
-/* ts_decode_attn that also records `ev_begin` just before and `ev_end` just
- * after its main (KV-streaming) kernel on the same stream, so the caller can
- * time that kernel alone with ts_event_elapsed_ms().  Events come from
- * ts_event_create(); either may be NULL. */
+/* ts_decode_attn whose main (KV-streaming) kernel is launched with `ev_begin`
+ * and `ev_end` attached to its dispatch: they take the kernel's own start and
+ * end timestamps, so ts_event_elapsed_ms() gives that kernel's duration alone.
+ * Events come from ts_event_create(); either may be NULL. */
 int ts_decode_attn_events(const ts_attn_shape *shape, const void *q, const void *k_pages,
                           const void *v_pages, const int32_t *page_table,
                           const int32_t *ctx_lens, const int32_t *q_lens, void *out,

@@ -164,6 +164,13 @@ def _check_tensors(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out):
         raise ValueError("out must match q and v_pages must match k_pages")
 
 
+def new_workspace(nbytes: int, device="cuda"):
+    """A zero-filled workspace of nbytes (the library requires zeros before
+    the first use and leaves its split counters zero after every call)."""
+    import torch
+    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
+
+
 def decode_attn(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale: float,
                 workspace=None, max_ctx_len: Optional[int] = None, num_workers: int = 0,
                 stream=None, events=None, variant: int = 0):
@@ -175,8 +182,11 @@ def decode_attn(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale: f
     _check_tensors(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out)
     shape = shape_of(q, k_pages, page_table, max_ctx_len, num_workers, variant)
     need = workspace_size(shape)
-    if workspace is None or workspace.numel() * workspace.element_size() < need:
-        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    if workspace is None:
+        workspace = new_workspace(need, q.device)
+    elif workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace has {workspace.numel() * workspace.element_size()} bytes, "
+                         f"this call needs {need}")
     args = (ctypes.byref(shape), q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
             page_table.data_ptr(), ctx_lens.data_ptr(), q_lens.data_ptr(), out.data_ptr(),
             ctypes.c_float(scale), workspace.data_ptr(),

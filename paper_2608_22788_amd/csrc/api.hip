@@ -1,6 +1,7 @@
 // api.hip -- host side of libtsattn: shape validation, kernel selection,
 // the work-partition size, launches and error reporting behind the C ABI
 // declared in include/ts_attn.h.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -22,7 +23,7 @@ kernel_fn verify_variant(int D, int NB);
 kernel_fn verify_team_variant(int rows, int *lds_bytes, int *nbe);
 kernel_fn merge_variant(int D);
 int debug_check(const ts_attn_shape *s, const int32_t *page_table, const int32_t *ctx_lens,
-                const int32_t *q_lens, hipStream_t stream);
+                const int32_t *q_lens, const int *counters, hipStream_t stream);
 
 static thread_local std::string g_last_error;
 
@@ -73,7 +74,7 @@ struct Plan {
     bool team;        // verify by four-wavefront teams sharing pages in LDS (head_dim 128)
     bool auto_w;      // worker count chosen by the library (W is then an upper bound)
     int G, NB, rows_per_unit, W;
-    size_t ws_o_bytes, ws_lse_off, ws_bytes;
+    size_t ws_cnt_off, ws_o_off, ws_lse_off, ws_bytes;
 };
 
 // Number of workers sharing the KV stream.  MI355X has 256 compute units.
@@ -137,6 +138,9 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
     if (s->num_kv_heads < 1 || s->num_q_heads < 1 || s->num_q_heads % s->num_kv_heads)
         return fail(TS_ERR_SHAPE, "num_q_heads %d must be a positive multiple of num_kv_heads %d",
                     s->num_q_heads, s->num_kv_heads);
+    if ((int64_t)s->num_seqs * s->num_kv_heads > kMaxUnits)
+        return fail(TS_ERR_SHAPE, "num_seqs * num_kv_heads = %lld exceeds %d",
+                    (long long)s->num_seqs * s->num_kv_heads, kMaxUnits);
     if (s->head_dim != 64 && s->head_dim != 128)
         return fail(TS_ERR_SHAPE, "head_dim %d unsupported (64 or 128)", s->head_dim);
     if (s->page_size != kPage)
@@ -172,9 +176,14 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
                (s->variant == TS_VARIANT_TEAM || (s->variant == TS_VARIANT_AUTO && pl->NB >= 2));
     pl->auto_w = s->num_workers == 0;
     pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team, pl->NB);
+    // Workspace: the split counters first, at a fixed size whatever the shape,
+    // so that no call's partial results ever land on them; then the partial
+    // outputs and their log-sum-exp.
     const size_t slots = 2 * (size_t)pl->W;
-    pl->ws_o_bytes = slots * pl->rows_per_unit * s->head_dim * sizeof(float);
-    pl->ws_lse_off = (pl->ws_o_bytes + 255) & ~(size_t)255;
+    pl->ws_cnt_off = 0;
+    pl->ws_o_off = kCounterBytes;
+    const size_t o_bytes = slots * pl->rows_per_unit * s->head_dim * sizeof(float);
+    pl->ws_lse_off = pl->ws_o_off + ((o_bytes + 255) & ~(size_t)255);
     pl->ws_bytes = pl->ws_lse_off + ((slots * pl->rows_per_unit * sizeof(float) + 255) & ~(size_t)255);
     return TS_OK;
 }
@@ -213,8 +222,9 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
         return st;
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
 
+    int *counters = reinterpret_cast<int *>(static_cast<char *>(workspace) + pl.ws_cnt_off);
     if (debug_enabled()) {
-        st = debug_check(s, page_table, ctx_lens, q_lens, hs);
+        st = debug_check(s, page_table, ctx_lens, q_lens, counters, hs);
         if (st)
             return st;
     }
@@ -227,8 +237,9 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
     p.ctx_lens = ctx_lens;
     p.q_lens = q_lens;
     p.out = static_cast<uint16_t *>(out);
-    p.ws_o = static_cast<float *>(workspace);
+    p.ws_o = reinterpret_cast<float *>(static_cast<char *>(workspace) + pl.ws_o_off);
     p.ws_lse = reinterpret_cast<float *>(static_cast<char *>(workspace) + pl.ws_lse_off);
+    p.counters = counters;
     p.B = s->num_seqs;
     p.Hq = s->num_q_heads;
     p.Hkv = s->num_kv_heads;
@@ -267,13 +278,21 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
     }
 
     hipError_t e;
-    if (ev_begin && (e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_begin), hs)) != hipSuccess)
-        return hip_fail(e, "hipEventRecord");
-    hipLaunchKernelGGL(main_k, dim3(pl.W), dim3(main_threads), main_lds, hs, p);
+    if (ev_begin || ev_end) {
+        // the events take the kernel's own start and end timestamps
+        void *args[] = {&p};
+        e = hipExtLaunchKernel(reinterpret_cast<const void *>(main_k), dim3(pl.W), dim3(main_threads), args,
+                               main_lds, hs, reinterpret_cast<hipEvent_t>(ev_begin),
+                               reinterpret_cast<hipEvent_t>(ev_end), 0);
+        if (e != hipSuccess)
+            return hip_fail(e, "attention kernel launch");
+    } else {
+        hipLaunchKernelGGL(main_k, dim3(pl.W), dim3(main_threads), main_lds, hs, p);
+    }
     if ((e = hipGetLastError()) != hipSuccess)
         return hip_fail(e, "attention kernel launch");
-    if (ev_end && (e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev_end), hs)) != hipSuccess)
-        return hip_fail(e, "hipEventRecord");
+    if (pl.q1)
+        return TS_OK;   // the decode kernel combines its own splits
     const int ngroups = (pl.rows_per_unit + 3) / 4;
     const unsigned merge_blocks = (unsigned)(p.B * p.Hkv * ngroups);
     hipLaunchKernelGGL(merge_k, dim3(merge_blocks), dim3(4 * kWave), lds, hs, p);

@@ -12,8 +12,10 @@
 // end inside a unit; such a piece is a split whose normalised partial output
 // and log2-sum-exp go to the workspace, slot 2w if the piece is the first of
 // the worker's range and 2w+1 otherwise.  A unit processed whole by one worker
-// is written straight to `out`.  The merge kernel finds the workers that
-// touched a unit by inverting the range formula and combines their slots.
+// is written straight to `out`.  The workers that touched a unit are found by
+// inverting the range formula, and their slots are combined (attn_split.h):
+// by the last of them to finish (one-token decode kernel) or by a separate
+// merge kernel (verify kernels).
 // Everything depends on ctx_lens / q_lens read on the device, so the launch
 // grid depends on the shape alone.
 #pragma once
@@ -26,6 +28,8 @@ namespace tsattn {
 constexpr int kPage = 16;          // tokens per page
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kMaxSeqs = 4096;     // sequences per call (LDS prefix array)
+constexpr int kMaxUnits = 1 << 18; // (sequence, KV head) units per call
+constexpr size_t kCounterBytes = (size_t)kMaxUnits * sizeof(int);   // split counters
 constexpr float kRescaleSlack = 8.0f;  // lazy rescale threshold, log2 units
 
 struct AttnParams {
@@ -38,6 +42,7 @@ struct AttnParams {
     uint16_t *out;              // [B][Qmax][Hq][D] bf16
     float *ws_o;                // [2W][rows_per_unit][D] fp32 partial outputs
     float *ws_lse;              // [2W][rows_per_unit] fp32 log2-sum-exp
+    int *counters;              // [B][Hkv] arrivals per split unit (zero between calls)
     int B, Hq, Hkv, D, Qmax, max_pages;
     int G;                      // Hq / Hkv
     int rows_per_unit;          // G * Qmax
@@ -200,6 +205,8 @@ struct Segment {
     int b, g;          // unit
     int j0, j1;        // logical pages [j0, j1) of the unit
     bool whole;        // the unit is entirely inside this segment
+    int np;            // pages of the unit
+    int64_t us;        // global index of the unit's first page
     int64_t next;      // global page after the segment
 };
 
@@ -216,6 +223,8 @@ __device__ __forceinline__ Segment locate(const AttnParams &p, const int *s_pre,
     const int64_t seg_end = unit_end < range_end ? unit_end : range_end;
     s.j1 = s.j0 + (int)(seg_end - x);
     s.whole = (s.j0 == 0) && (seg_end == unit_end);
+    s.np = np;
+    s.us = base + (int64_t)s.g * np;
     s.next = seg_end;
     return s;
 }

@@ -23,10 +23,18 @@
 //     pair; the row sum is accumulated from the same rounded probabilities;
 //   * at the end of a segment the 8 slots are merged with log-sum-exp
 //     weights through cross-lane shuffles.
+// Splits are combined in this kernel: a wavefront that wrote a partial (a
+// piece of a unit that other workers share) with device-coherent stores waits
+// for them to complete, then counts its arrival on the unit's counter; the one
+// that arrives last combines all partials of the unit (device-coherent
+// loads), writes the output rows and sets the counter back to zero.  No
+// cache-wide write-back or invalidation is needed.  Each unit has 2 pieces
+// (rarely more) at the usual sizes, so this costs the last arriver one extra
+// read of a few KiB, where a separate merge kernel would cost a launch.
 // Masking: only the last page of a sequence has slots past the context end;
 // their probabilities are forced to 0 and their value rows to 0, so stale
 // data (even NaN) in unused slots never reaches the output.
-#include "attn_common.h"
+#include "attn_split.h"
 
 #include <type_traits>
 
@@ -169,7 +177,35 @@ struct DecodeQ1 {
         }
     }
 
-    __device__ static void segment(const AttnParams &p, const Segment &s, int slot_id) {
+    // The last worker to finish a piece of the unit combines all pieces.  The
+    // partials were written with device-coherent stores; once they are
+    // complete (vector memory counter drained) the arrival is counted, and
+    // the last arriver reads the others' partials with device-coherent loads
+    // issued after its count returned.
+    __device__ static void arrive(const AttnParams &p, const Segment &s, int64_t ptot, int lane) {
+        wait_vmem();
+        int *cnt = p.counters + (size_t)s.b * p.Hkv + s.g;
+        int old = 0;
+        if (lane == 0)
+            old = atomicAdd(cnt, 1);
+        old = first_lane_int(old);
+        const UnitSplit u = unit_split(ptot, s.us, s.np, p.W);
+        if (old != u.nparts - 1)
+            return;
+        const int part = lane & 15;
+#pragma unroll
+        for (int r0 = 0; r0 < G; r0 += 4) {
+            const int r = r0 + (lane >> 4);
+            Acc<D / 16> a;
+            a.init();
+            gather_partials<D, true>(p, u, r < G ? r : 0, part, 0, 1, a);
+            if (r < G)
+                write_merged<D>(p, s.b, s.g, r, part, a);
+        }
+        __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+
+    __device__ static void segment(const AttnParams &p, const Segment &s, int slot_id, int64_t ptot) {
         const int lane = threadIdx.x;
         const int slot = lane >> 3;
         const int part = lane & 7;
@@ -260,22 +296,22 @@ struct DecodeQ1 {
                         *reinterpret_cast<uint4 *>(dst + 64 * c + 8 * part) = w4;
                     }
                 } else {
+                    // device-coherent stores: another worker of this launch
+                    // may combine them (see arrive)
                     const size_t row = (size_t)slot_id * p.rows_per_unit + r;
                     float *dst = p.ws_o + row * D;
 #pragma unroll
-                    for (int c = 0; c < NC; c++) {
-                        float4 lo = make_float4(o[r][8 * c + 0] * inv, o[r][8 * c + 1] * inv,
-                                                o[r][8 * c + 2] * inv, o[r][8 * c + 3] * inv);
-                        float4 hi = make_float4(o[r][8 * c + 4] * inv, o[r][8 * c + 5] * inv,
-                                                o[r][8 * c + 6] * inv, o[r][8 * c + 7] * inv);
-                        *reinterpret_cast<float4 *>(dst + 64 * c + 8 * part) = lo;
-                        *reinterpret_cast<float4 *>(dst + 64 * c + 8 * part + 4) = hi;
-                    }
+                    for (int c = 0; c < NC; c++)
+#pragma unroll
+                        for (int e = 0; e < 8; e++)
+                            st_coherent(dst + 64 * c + 8 * part + e, o[r][8 * c + e] * inv);
                     if (part == 0)
-                        p.ws_lse[row] = l > 0.0f ? M + __log2f(l) : -INFINITY;
+                        st_coherent(p.ws_lse + row, l > 0.0f ? M + __log2f(l) : -INFINITY);
                 }
             }
         }
+        if (!s.whole)
+            arrive(p, s, ptot, lane);
     }
 };
 
@@ -289,7 +325,7 @@ __global__ __launch_bounds__(64) void decode_q1_kernel(AttnParams p) {
     const int64_t end = worker_begin(ptot, w + 1, p.W);
     for (int64_t x = begin; x < end;) {
         const Segment s = locate(p, s_pre, x, end);
-        DecodeQ1<D, G>::segment(p, s, x == begin ? 2 * w : 2 * w + 1);
+        DecodeQ1<D, G>::segment(p, s, x == begin ? 2 * w : 2 * w + 1, ptot);
         x = s.next;
     }
 }

@@ -113,6 +113,8 @@ int run_point(const ts_sweep_config &c, int32_t batch, int32_t seed, hipStream_t
         (st = dq.alloc((size_t)batch * 4, "hipMalloc(q_lens)")))
         return st;
     hipError_t e;
+    if ((e = hipMemsetAsync(ws.p, 0, ws_bytes, stream)))   // zero before its first use
+        return hip_fail(e, "hipMemsetAsync(workspace)");
     if ((e = hipMemcpyAsync(dtab.p, table.data(), table.size() * 4, hipMemcpyHostToDevice, stream)) ||
         (e = hipMemcpyAsync(dlen.p, lens.data(), (size_t)batch * 4, hipMemcpyHostToDevice, stream)) ||
         (e = hipMemcpyAsync(dq.p, qlens.data(), (size_t)batch * 4, hipMemcpyHostToDevice, stream)))

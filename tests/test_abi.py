@@ -47,7 +47,7 @@ def base_shape(**kw):
     dict(num_kv_heads=0), dict(head_dim=96), dict(head_dim=256), dict(max_q_len=0),
     dict(max_q_len=17), dict(num_q_heads=32, num_kv_heads=1, max_q_len=4),
     dict(max_pages_per_seq=0), dict(max_ctx_len=257), dict(max_ctx_len=0), dict(num_pages=0),
-    dict(num_workers=-1)])
+    dict(num_workers=-1), dict(num_seqs=4096, num_q_heads=128, num_kv_heads=128)])
 def test_bad_shapes_rejected(kw):
     s = base_shape(**kw)
     assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) == 0

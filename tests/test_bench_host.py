@@ -1,0 +1,49 @@
+"""Host-side logic of bench.py (no GPU): the single-GPU guard, the sweep
+aggregation over seeds, and the rule that a committed traffic figure counts
+only for the kernel sources it was measured on."""
+import importlib.util
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def bench():
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=60)
+    assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_sweep_summary_aggregates_over_seeds(bench):
+    pts = [dict(batch=b, q_len=4 if b <= 8 else 1, seed=s, kv_gbps=100.0 * b + s,
+                hbm_frac=(100.0 * b + s) / 8000, tokens_per_s=10.0 * s, tau_us=1.0 + s)
+           for b in (8, 16) for s in range(5)]
+    out = bench.sweep_summary(pts)
+    assert [r["batch"] for r in out] == [8, 16]
+    r = out[0]
+    assert r["seeds"] == 5 and r["q_len"] == 4
+    assert r["kv_gbps"] == 802.0 and r["kv_gbps_min"] == 800.0 and r["kv_gbps_max"] == 804.0
+    assert r["tau_us"] == 3.0 and r["tau_us_min"] == 1.0 and r["tau_us_max"] == 5.0
+
+
+def test_traffic_counts_only_for_matching_sources(bench, tmp_path, monkeypatch):
+    h = bench.kernel_hash("dflash")
+    f = tmp_path / "t.md"
+    f.write_text(f"traffic dflash kernel_hash={h} bytes_per_launch=123\n"
+                 f"traffic mtp kernel_hash=0000000000000000 bytes_per_launch=456\n")
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
+    assert bench.measured_traffic("dflash") == 123
+    assert bench.measured_traffic("mtp") is None        # stale: sources changed since
+    assert bench.measured_traffic("bulk") is None       # never measured
+    assert len(h) == 16 and h != bench.kernel_hash("bulk")

@@ -108,6 +108,29 @@ def test_many_sequences(dev, orc, B, Qmax):
     run_case(dev, orc, wl, workers=(0, 5, 2000))
 
 
+def test_workspace_reused_across_calls_and_shapes(dev, orc):
+    """One zero-filled workspace serves a run of calls of different shapes and
+    worker counts; each result matches the oracle, and after every call the
+    per-unit arrival counters (the first B * Hkv int32 of the workspace) are
+    zero again."""
+    import torch
+    from paper_2608_22788_amd import binding
+    _, device = dev
+    ws = binding.new_workspace(64 << 20)
+    cases = [(32, 8, 128, [1] * 5, [1, 15, 16, 33, 1000], 0), (8, 2, 64, [1] * 3, [16, 17, 300], 3),
+             (32, 8, 128, [4, 4], [500, 77], 0), (32, 8, 128, [1] * 40, [130] * 40, 300),
+             (16, 2, 128, [1, 1, 1], [64, 65, 511], 1)]
+    for n, (Hq, Hkv, D, ql, cl, w) in enumerate(cases):
+        wl = synth.make_workload(f"reuse{n}", seed=40 + n, cfg=small_cfg(Hq, Hkv, D), ctx_lens=cl, q_lens=ql)
+        ref = oracle_out(orc, wl)
+        t = device.upload(wl)
+        say(f"reuse case {n}: B={wl.B} Hq={Hq} Hkv={Hkv} D={D} workers={w}")
+        device.run(wl, t, num_workers=w, workspace=ws)
+        assert_parity(device.out_as_f64(t), ref, f"reuse{n}")
+        torch.cuda.synchronize()
+        assert int(ws[:1 << 20].count_nonzero()) == 0, f"counters left set after case {n}"
+
+
 def test_one_key_returns_value_row_bitwise(dev, orc):
     _, device = dev
     for Qmax, var in ((1, 0), (2, 1), (2, 2)):

@@ -1,6 +1,7 @@
 """Runtime contracts of the C ABI on the GPU: a call can be captured into a
 HIP graph and replayed, and TS_DEBUG=1 turns violated device-side
-preconditions into TS_ERR_SHAPE before any attention kernel runs."""
+preconditions into TS_ERR_SHAPE (a workspace whose counters are not zero
+into TS_ERR_WORKSPACE) before any attention kernel runs."""
 import os
 import subprocess
 import sys
@@ -31,7 +32,7 @@ def test_graph_capture_replays_match_eager(q_lens, ctx):
     wl = synth.make_workload("graph", seed=3, cfg=small_cfg(32, 8, 128), ctx_lens=ctx, q_lens=q_lens)
     t = device.upload(wl)
     shape = binding.shape_of(t["q"], t["k_pages"], t["page_table"], wl.max_ctx_len)
-    ws = torch.empty(binding.workspace_size(shape), dtype=torch.uint8, device="cuda")
+    ws = binding.new_workspace(binding.workspace_size(shape))
     device.run(wl, t, workspace=ws)                    # eager reference (and device check)
     torch.cuda.synchronize()
     ref = t["out"].clone()
@@ -74,6 +75,17 @@ DEBUG_SCRIPT = textwrap.dedent("""
         device.run(wl, t3); results.append("no error")
     except binding.TsError as e:
         results.append(str(e.status) + ":" + str(e))
+    # a reused workspace passes the check after every call (its counters are
+    # left zero); one that was never zero-filled is reported
+    ws = binding.new_workspace(8 << 20)
+    for _ in range(3):
+        device.run(wl, t, num_workers=7, workspace=ws)
+    torch.cuda.synchronize()
+    dirty = torch.full((8 << 20,), 1, dtype=torch.uint8, device="cuda")
+    try:
+        device.run(wl, t, workspace=dirty); results.append("no error")
+    except binding.TsError as e:
+        results.append(str(e.status) + ":" + str(e))
     print("RESULTS", results)
 """)
 
@@ -87,3 +99,4 @@ def test_debug_mode_reports_bad_device_inputs():
     line = [ln for ln in r.stdout.splitlines() if ln.startswith("RESULTS")][0]
     assert "-2:" in line.split("'")[1] and "page id" in line
     assert line.count("-2:") == 2 and "q_lens" in line
+    assert line.count("-3:") == 1 and "zero-fill" in line
