@@ -140,8 +140,8 @@ int ts_decode_attn_events(const ts_attn_shape *shape, const void *q, const void 
  * 65536, the same SplitMix64 definitions as the test generator), a random
  * page permutation and N(0,1) bf16 values, then times ts_decode_attn with HIP
  * events while rotating over enough distinct KV pools to defeat the
- * last-level cache.  Synchronous; allocates and frees its own device memory
- * on the current device. */
+ * last-level cache.  Synchronous; allocates its device memory once, at the
+ * largest point's size, on the current device, and frees it on return. */
 typedef struct ts_sweep_config {
     int32_t num_q_heads;        /* 32 */
     int32_t num_kv_heads;       /* 8 */

@@ -78,22 +78,22 @@ struct Plan {
 };
 
 // Number of workers sharing the KV stream.  MI355X has 256 compute units.
-// Measured on the bulk, MTP and block-draft workloads, the best count is one
-// full round of resident workers: all of them start together and finish
-// together, where a partial second round leaves most of the chip idle at the
-// end.  The table below is the measured residency per compute unit (it also
-// bounds the workspace); at launch the auto count is further capped by the
-// occupancy the HIP runtime reports for the compiled kernel.
-static int per_cu_bound(bool q1, bool team, int NB) {
+// Measured (after a clock warm-up of a few hundred calls) on the bulk, MTP and
+// block-draft workloads: the decode kernel is best with 4 single-wavefront
+// workers per compute unit (1024), the single-wavefront verify kernel with 3
+// (768; 1024 is within 1 %), and the team verify kernel with 2 teams per
+// compute unit (512), although its registers would allow 3: the third team
+// lowers throughput by 8 %.  The auto count is further capped at launch by
+// the occupancy the HIP runtime reports for the compiled kernel, so all
+// workers run in one round.
+static int per_cu_bound(bool q1, bool team) {
     if (q1)
-        return 4;              // decode: 4 single-wavefront workers
-    if (team)
-        return NB >= 3 ? 3 : 2;   // 64 rows: 3 teams (166 VGPRs); 16-32 rows: 2
-    return 4;                  // single-wavefront verify
+        return 4;
+    return team ? 2 : 3;
 }
 
-static int auto_workers(const ts_attn_shape *s, bool q1, bool team, int NB) {
-    int64_t w = 256LL * per_cu_bound(q1, team, NB);
+static int auto_workers(const ts_attn_shape *s, bool q1, bool team) {
+    int64_t w = 256LL * per_cu_bound(q1, team);
     // Small shapes get fewer workers so that each has at least a few pages.
     const int64_t pages_ub = (int64_t)s->num_seqs * s->num_kv_heads *
                              ((s->max_ctx_len + kPage - 1) / kPage);
@@ -175,7 +175,7 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
     pl->team = !pl->q1 && s->head_dim == 128 &&
                (s->variant == TS_VARIANT_TEAM || (s->variant == TS_VARIANT_AUTO && pl->NB >= 2));
     pl->auto_w = s->num_workers == 0;
-    pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team, pl->NB);
+    pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team);
     // Workspace: the split counters first, at a fixed size whatever the shape,
     // so that no call's partial results ever land on them; then the partial
     // outputs and their log-sum-exp.
@@ -276,6 +276,9 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
             pl.W = resident;
         p.W = pl.W;
     }
+    // The one-token kernel combines its splits itself when there are at least
+    // twice as many units as workers (a unit then has one or two pieces).
+    p.fuse_splits = pl.q1 && (int64_t)p.B * p.Hkv >= 2 * (int64_t)p.W;
 
     hipError_t e;
     if (ev_begin || ev_end) {
@@ -291,8 +294,8 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
     }
     if ((e = hipGetLastError()) != hipSuccess)
         return hip_fail(e, "attention kernel launch");
-    if (pl.q1)
-        return TS_OK;   // the decode kernel combines its own splits
+    if (p.fuse_splits)
+        return TS_OK;   // the decode kernel combined its own splits
     const int ngroups = (pl.rows_per_unit + 3) / 4;
     const unsigned merge_blocks = (unsigned)(p.B * p.Hkv * ngroups);
     hipLaunchKernelGGL(merge_k, dim3(merge_blocks), dim3(4 * kWave), lds, hs, p);

@@ -14,8 +14,8 @@
 // the worker's range and 2w+1 otherwise.  A unit processed whole by one worker
 // is written straight to `out`.  The workers that touched a unit are found by
 // inverting the range formula, and their slots are combined (attn_split.h):
-// by the last of them to finish (one-token decode kernel) or by a separate
-// merge kernel (verify kernels).
+// by the last of them to finish (one-token decode kernel, many units) or by a
+// separate merge kernel.
 // Everything depends on ctx_lens / q_lens read on the device, so the launch
 // grid depends on the shape alone.
 #pragma once
@@ -47,6 +47,7 @@ struct AttnParams {
     int G;                      // Hq / Hkv
     int rows_per_unit;          // G * Qmax
     int W;                      // workers (wavefronts)
+    int fuse_splits;            // one-token kernel: combine splits in the kernel
     float scale_log2;           // scale * log2(e)
 };
 

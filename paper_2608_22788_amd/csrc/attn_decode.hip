@@ -23,14 +23,17 @@
 //     pair; the row sum is accumulated from the same rounded probabilities;
 //   * at the end of a segment the 8 slots are merged with log-sum-exp
 //     weights through cross-lane shuffles.
-// Splits are combined in this kernel: a wavefront that wrote a partial (a
-// piece of a unit that other workers share) with device-coherent stores waits
-// for them to complete, then counts its arrival on the unit's counter; the one
-// that arrives last combines all partials of the unit (device-coherent
-// loads), writes the output rows and sets the counter back to zero.  No
-// cache-wide write-back or invalidation is needed.  Each unit has 2 pieces
-// (rarely more) at the usual sizes, so this costs the last arriver one extra
-// read of a few KiB, where a separate merge kernel would cost a launch.
+// With p.fuse_splits set, splits are combined in this kernel: a wavefront
+// that wrote a partial (a piece of a unit that other workers share) with
+// device-coherent stores waits for them to complete, then counts its arrival
+// on the unit's counter; the one that arrives last combines all partials of
+// the unit (device-coherent loads), writes the output rows and sets the
+// counter back to zero.  No cache-wide write-back or invalidation is needed.
+// This saves the merge kernel's launch but puts four dependent memory round
+// trips (store, count, partial loads, output) at the end of the last pieces;
+// the host enables it when units are at least twice as many as workers (a
+// unit then has one or two pieces), where it was measured faster (4-5 % at
+// 256 sequences), and otherwise launches the merge kernel.
 // Masking: only the last page of a sequence has slots past the context end;
 // their probabilities are forced to 0 and their value rows to 0, so stale
 // data (even NaN) in unused slots never reaches the output.
@@ -296,21 +299,36 @@ struct DecodeQ1 {
                         *reinterpret_cast<uint4 *>(dst + 64 * c + 8 * part) = w4;
                     }
                 } else {
-                    // device-coherent stores: another worker of this launch
-                    // may combine them (see arrive)
                     const size_t row = (size_t)slot_id * p.rows_per_unit + r;
                     float *dst = p.ws_o + row * D;
+                    const float lse = l > 0.0f ? M + __log2f(l) : -INFINITY;
+                    if (p.fuse_splits) {
+                        // device-coherent stores: another worker of this
+                        // launch may combine them (see arrive)
 #pragma unroll
-                    for (int c = 0; c < NC; c++)
+                        for (int c = 0; c < NC; c++)
 #pragma unroll
-                        for (int e = 0; e < 8; e++)
-                            st_coherent(dst + 64 * c + 8 * part + e, o[r][8 * c + e] * inv);
-                    if (part == 0)
-                        st_coherent(p.ws_lse + row, l > 0.0f ? M + __log2f(l) : -INFINITY);
+                            for (int e = 0; e < 8; e++)
+                                st_coherent(dst + 64 * c + 8 * part + e, o[r][8 * c + e] * inv);
+                        if (part == 0)
+                            st_coherent(p.ws_lse + row, lse);
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < NC; c++) {
+                            float4 lo = make_float4(o[r][8 * c + 0] * inv, o[r][8 * c + 1] * inv,
+                                                    o[r][8 * c + 2] * inv, o[r][8 * c + 3] * inv);
+                            float4 hi = make_float4(o[r][8 * c + 4] * inv, o[r][8 * c + 5] * inv,
+                                                    o[r][8 * c + 6] * inv, o[r][8 * c + 7] * inv);
+                            *reinterpret_cast<float4 *>(dst + 64 * c + 8 * part) = lo;
+                            *reinterpret_cast<float4 *>(dst + 64 * c + 8 * part + 4) = hi;
+                        }
+                        if (part == 0)
+                            p.ws_lse[row] = lse;
+                    }
                 }
             }
         }
-        if (!s.whole)
+        if (!s.whole && p.fuse_splits)
             arrive(p, s, ptot, lane);
     }
 };

@@ -65,71 +65,88 @@ double quantile(std::vector<double> v, double q) {
     return v[lo] + (pos - (double)lo) * (v[hi] - v[lo]);
 }
 
-int run_point(const ts_sweep_config &c, int32_t batch, int32_t seed, hipStream_t stream,
-              ts_sweep_point *pt) {
-    const int32_t Q = batch <= c.verify_max_batch ? c.verify_q_len : 1;
-    std::vector<int32_t> lens((size_t)batch), qlens((size_t)batch, Q);
-    sweep_lengths(batch, (uint64_t)seed, lens.data());
-    int32_t maxp = 1, maxl = 1;
-    int64_t total_pages = 0, sum_ctx = 0;
-    for (int32_t L : lens) {
-        maxp = std::max(maxp, (L + 15) / 16);
-        maxl = std::max(maxl, L);
-        total_pages += (L + 15) / 16;
-        sum_ctx += L;
+// Host description of one sweep point.
+struct Point {
+    int32_t batch, seed, Q, maxp, maxl;
+    int64_t total_pages, sum_ctx, pools, pool_bytes;
+    std::vector<int32_t> lens, qlens, table;
+    ts_attn_shape sh;
+    size_t ws_bytes;
+};
+
+int plan_point(const ts_sweep_config &c, int32_t batch, int32_t seed, Point *pt) {
+    Point &P = *pt;
+    P.batch = batch;
+    P.seed = seed;
+    P.Q = batch <= c.verify_max_batch ? c.verify_q_len : 1;
+    P.lens.assign((size_t)batch, 0);
+    P.qlens.assign((size_t)batch, P.Q);
+    sweep_lengths(batch, (uint64_t)seed, P.lens.data());
+    P.maxp = 1;
+    P.maxl = 1;
+    P.total_pages = 0;
+    P.sum_ctx = 0;
+    for (int32_t L : P.lens) {
+        P.maxp = std::max(P.maxp, (L + 15) / 16);
+        P.maxl = std::max(P.maxl, L);
+        P.total_pages += (L + 15) / 16;
+        P.sum_ctx += L;
     }
-    std::vector<int32_t> table((size_t)batch * maxp);
-    int st = build_page_table(batch, lens.data(), 16, maxp, (uint64_t)seed, table.data());
+    P.table.assign((size_t)batch * P.maxp, 0);
+    int st = build_page_table(batch, P.lens.data(), 16, P.maxp, (uint64_t)seed, P.table.data());
     if (st)
         return st;
+    const int64_t pool_elems = P.total_pages * c.num_kv_heads * 16 * c.head_dim;
+    P.pool_bytes = pool_elems * 2;                  // one of K or V
+    P.pools = (c.min_rotation_bytes + 2 * P.pool_bytes - 1) / (2 * P.pool_bytes);
+    P.pools = std::max<int64_t>(1, std::min<int64_t>(P.pools, 512));
+    P.sh = ts_attn_shape{};
+    P.sh.num_seqs = batch;
+    P.sh.num_q_heads = c.num_q_heads;
+    P.sh.num_kv_heads = c.num_kv_heads;
+    P.sh.head_dim = c.head_dim;
+    P.sh.page_size = 16;
+    P.sh.max_q_len = P.Q;
+    P.sh.max_pages_per_seq = P.maxp;
+    P.sh.max_ctx_len = P.maxl;
+    P.sh.num_pages = P.total_pages;
+    P.ws_bytes = ts_decode_attn_workspace_size(&P.sh);
+    return P.ws_bytes ? TS_OK : TS_ERR_SHAPE;
+}
 
-    const int64_t pool_elems = total_pages * c.num_kv_heads * 16 * c.head_dim;
-    const int64_t pool_bytes = pool_elems * 2;                  // one of K or V
-    int64_t pools = (c.min_rotation_bytes + 2 * pool_bytes - 1) / (2 * pool_bytes);
-    pools = std::max<int64_t>(1, std::min<int64_t>(pools, 512));
+// Device memory for every point of a sweep, allocated once at the largest
+// size (memory obtained again from the driver after a free can stream a few
+// per cent slower, which would bias later points).
+struct Arena {
+    DevBuf kv, q, out, ws, tab, len, ql;
+    size_t kv_bytes = 0;
+};
 
-    ts_attn_shape sh = {};
-    sh.num_seqs = batch;
-    sh.num_q_heads = c.num_q_heads;
-    sh.num_kv_heads = c.num_kv_heads;
-    sh.head_dim = c.head_dim;
-    sh.page_size = 16;
-    sh.max_q_len = Q;
-    sh.max_pages_per_seq = maxp;
-    sh.max_ctx_len = maxl;
-    sh.num_pages = total_pages;
-    const size_t ws_bytes = ts_decode_attn_workspace_size(&sh);
-    if (!ws_bytes)
-        return TS_ERR_SHAPE;
-
-    DevBuf k, v, q, out, ws, dtab, dlen, dq;
+int run_point(const ts_sweep_config &c, const Point &P, Arena &A, hipStream_t stream,
+              ts_sweep_point *pt) {
+    const int32_t batch = P.batch, Q = P.Q;
+    const int64_t pools = P.pools, pool_bytes = P.pool_bytes;
+    const int64_t pool_elems = pool_bytes / 2;
+    char *kbase = static_cast<char *>(A.kv.p);
+    char *vbase = kbase + (size_t)(pool_bytes * pools);
     const size_t qelems = (size_t)batch * Q * c.num_q_heads * c.head_dim;
-    if ((st = k.alloc((size_t)(pool_bytes * pools), "hipMalloc(K pools)")) ||
-        (st = v.alloc((size_t)(pool_bytes * pools), "hipMalloc(V pools)")) ||
-        (st = q.alloc(qelems * 2, "hipMalloc(q)")) || (st = out.alloc(qelems * 2, "hipMalloc(out)")) ||
-        (st = ws.alloc(ws_bytes, "hipMalloc(workspace)")) ||
-        (st = dtab.alloc(table.size() * 4, "hipMalloc(page table)")) ||
-        (st = dlen.alloc((size_t)batch * 4, "hipMalloc(ctx_lens)")) ||
-        (st = dq.alloc((size_t)batch * 4, "hipMalloc(q_lens)")))
-        return st;
     hipError_t e;
-    if ((e = hipMemsetAsync(ws.p, 0, ws_bytes, stream)))   // zero before its first use
-        return hip_fail(e, "hipMemsetAsync(workspace)");
-    if ((e = hipMemcpyAsync(dtab.p, table.data(), table.size() * 4, hipMemcpyHostToDevice, stream)) ||
-        (e = hipMemcpyAsync(dlen.p, lens.data(), (size_t)batch * 4, hipMemcpyHostToDevice, stream)) ||
-        (e = hipMemcpyAsync(dq.p, qlens.data(), (size_t)batch * 4, hipMemcpyHostToDevice, stream)))
+    int st;
+    if ((e = hipMemcpyAsync(A.tab.p, P.table.data(), P.table.size() * 4, hipMemcpyHostToDevice, stream)) ||
+        (e = hipMemcpyAsync(A.len.p, P.lens.data(), (size_t)batch * 4, hipMemcpyHostToDevice, stream)) ||
+        (e = hipMemcpyAsync(A.ql.p, P.qlens.data(), (size_t)batch * 4, hipMemcpyHostToDevice, stream)))
         return hip_fail(e, "hipMemcpyAsync(sweep inputs)");
-    if ((st = synth_fill(k.p, pool_elems * pools, (uint64_t)seed, kStreamK, 0, stream)) ||
-        (st = synth_fill(v.p, pool_elems * pools, (uint64_t)seed, kStreamV, 0, stream)) ||
-        (st = synth_fill(q.p, (int64_t)qelems, (uint64_t)seed, kStreamQ, 0, stream)))
+    if ((st = synth_fill(kbase, pool_elems * pools, (uint64_t)P.seed, kStreamK, 0, stream)) ||
+        (st = synth_fill(vbase, pool_elems * pools, (uint64_t)P.seed, kStreamV, 0, stream)) ||
+        (st = synth_fill(A.q.p, (int64_t)qelems, (uint64_t)P.seed, kStreamQ, 0, stream)))
         return st;
 
     const float scale = 1.0f / std::sqrt((float)c.head_dim);
     auto call = [&](int64_t i) {
         const size_t off = (size_t)((i % pools) * pool_bytes);
-        return ts_decode_attn(&sh, q.p, static_cast<char *>(k.p) + off, static_cast<char *>(v.p) + off,
-                              static_cast<const int32_t *>(dtab.p), static_cast<const int32_t *>(dlen.p),
-                              static_cast<const int32_t *>(dq.p), out.p, scale, ws.p, ws_bytes, stream);
+        return ts_decode_attn(&P.sh, A.q.p, kbase + off, vbase + off, static_cast<const int32_t *>(A.tab.p),
+                              static_cast<const int32_t *>(A.len.p), static_cast<const int32_t *>(A.ql.p),
+                              A.out.p, scale, A.ws.p, P.ws_bytes, stream);
     };
     for (int i = 0; i < c.warmup; i++)
         if ((st = call(i)))
@@ -158,10 +175,10 @@ int run_point(const ts_sweep_config &c, int32_t batch, int32_t seed, hipStream_t
     }
     pt->batch = batch;
     pt->q_len = Q;
-    pt->seed = seed;
+    pt->seed = P.seed;
     pt->num_pools = (int32_t)pools;
-    pt->sum_ctx = sum_ctx;
-    pt->kv_bytes = sum_ctx * c.num_kv_heads * c.head_dim * 2 * 2;
+    pt->sum_ctx = P.sum_ctx;
+    pt->kv_bytes = P.sum_ctx * c.num_kv_heads * c.head_dim * 2 * 2;
     pt->t_median_us = quantile(us, 0.5);
     pt->t_p10_us = quantile(us, 0.1);
     pt->t_p90_us = quantile(us, 0.9);
@@ -196,18 +213,39 @@ extern "C" int ts_concurrency_sweep(const ts_sweep_config *cfg, ts_sweep_point *
     if (st)
         return st;
     try {
+        // plan every point on the host, then size one arena for the largest
+        std::vector<Point> plan((size_t)c.num_batches * c.num_seeds);
+        size_t kv = 0, qe = 0, ws = 0, tab = 0, bmax = 0;
+        for (int i = 0; i < c.num_batches; i++) {
+            for (int seed = 0; seed < c.num_seeds; seed++) {
+                Point &P = plan[(size_t)i * c.num_seeds + seed];
+                if ((st = plan_point(c, c.batches[i], seed, &P)))
+                    return st;
+                kv = std::max(kv, (size_t)(2 * P.pool_bytes * P.pools));
+                qe = std::max(qe, (size_t)P.batch * P.Q * c.num_q_heads * c.head_dim);
+                ws = std::max(ws, P.ws_bytes);
+                tab = std::max(tab, P.table.size());
+                bmax = std::max(bmax, (size_t)P.batch);
+            }
+        }
+        Arena A;
         Stream s;
         hipError_t e = hipStreamCreate(&s.s);
         if (e != hipSuccess)
             return hip_fail(e, "hipStreamCreate");
+        if ((st = A.kv.alloc(kv, "hipMalloc(KV pools)")) || (st = A.q.alloc(qe * 2, "hipMalloc(q)")) ||
+            (st = A.out.alloc(qe * 2, "hipMalloc(out)")) || (st = A.ws.alloc(ws, "hipMalloc(workspace)")) ||
+            (st = A.tab.alloc(tab * 4, "hipMalloc(page table)")) ||
+            (st = A.len.alloc(bmax * 4, "hipMalloc(ctx_lens)")) ||
+            (st = A.ql.alloc(bmax * 4, "hipMalloc(q_lens)")))
+            return st;
+        if ((e = hipMemsetAsync(A.ws.p, 0, ws, s.s)))   // zero before its first use
+            return hip_fail(e, "hipMemsetAsync(workspace)");
         int32_t n = 0;
-        for (int i = 0; i < c.num_batches; i++) {
-            for (int seed = 0; seed < c.num_seeds; seed++) {
-                st = run_point(c, c.batches[i], seed, s.s, &pts[n]);
-                if (st)
-                    return st;
-                n++;
-            }
+        for (const Point &P : plan) {
+            if ((st = run_point(c, P, A, s.s, &pts[n])))
+                return st;
+            n++;
         }
         *n_out = n;
         return TS_OK;
