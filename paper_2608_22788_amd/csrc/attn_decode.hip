@@ -306,10 +306,14 @@ struct DecodeQ1 {
                         // device-coherent stores: another worker of this
                         // launch may combine them (see arrive)
 #pragma unroll
-                        for (int c = 0; c < NC; c++)
-#pragma unroll
-                            for (int e = 0; e < 8; e++)
-                                st_coherent(dst + 64 * c + 8 * part + e, o[r][8 * c + e] * inv);
+                        for (int c = 0; c < NC; c++) {
+                            const f32x4_t lo = {o[r][8 * c + 0] * inv, o[r][8 * c + 1] * inv,
+                                                o[r][8 * c + 2] * inv, o[r][8 * c + 3] * inv};
+                            const f32x4_t hi = {o[r][8 * c + 4] * inv, o[r][8 * c + 5] * inv,
+                                                o[r][8 * c + 6] * inv, o[r][8 * c + 7] * inv};
+                            st_coherent16(dst + 64 * c + 8 * part, lo);
+                            st_coherent16(dst + 64 * c + 8 * part + 4, hi);
+                        }
                         if (part == 0)
                             st_coherent(p.ws_lse + row, lse);
                     } else {

@@ -30,6 +30,13 @@ __device__ __forceinline__ float ld_coherent(const float *p) {
 __device__ __forceinline__ void st_coherent(float *p, float v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// 16-byte form of st_coherent (p 16-byte aligned).  The device-scope policy
+// bit is only reachable for vector stores through an instruction written out;
+// the data registers are read when the store issues, and wait_vmem() below
+// covers its completion.
+__device__ __forceinline__ void st_coherent16(float *p, f32x4_t v) {
+    asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+}
 // Waits until every vector memory operation this wavefront issued is complete.
 __device__ __forceinline__ void wait_vmem() {
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0); expcnt, lgkmcnt left at their maximum
