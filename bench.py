@@ -33,12 +33,13 @@ sys.path.insert(0, ROOT)
 
 PEAK_GBPS = 8000.0          # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.md")
-# Files whose content decides the streaming kernel of each workload; a traffic
-# figure counts only while their hash matches the one it was measured on.
+# Files whose content decides the streaming kernel of each workload and its
+# launch; a traffic figure counts only while their hash matches the one it was
+# measured on.
 TRAFFIC_SOURCES = {
-    "bulk": ["csrc/attn_common.h", "csrc/attn_decode.hip", "build.py"],
-    "mtp": ["csrc/attn_common.h", "csrc/attn_verify.hip", "build.py"],
-    "dflash": ["csrc/attn_common.h", "csrc/attn_verify_team.hip", "build.py"],
+    "bulk": ["csrc/attn_common.h", "csrc/attn_split.h", "csrc/attn_decode.hip", "csrc/api.hip", "build.py"],
+    "mtp": ["csrc/attn_common.h", "csrc/attn_verify.hip", "csrc/api.hip", "build.py"],
+    "dflash": ["csrc/attn_common.h", "csrc/attn_verify_team.hip", "csrc/api.hip", "build.py"],
 }
 KERNELS = {"bulk": "decode_q1_kernel<128,4>", "mtp": "verify_kernel<128,1>",
            "dflash": "verify_team_kernel<4>"}
