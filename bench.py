@@ -173,6 +173,23 @@ def cpu_baseline(wl, min_seconds=10.0, max_runs=50):
                        f"float64, {runs} runs, {dt:.3f} s each")
 
 
+def makespan_model(sweep, wl):
+    """The measured curve fed into the completion-time model (Sec. 2.1,
+    App. D): tau(b) = mean attention time per decoded position over the seeds,
+    tabulated for b = 1..512, then the bulk workload's lengths decoded on one
+    replica: its completion time and the share of the longest 5 % of requests."""
+    from paper_2608_22788_amd import binding
+    b = [r["batch"] for r in sweep]
+    tau = binding.tau_table(b, [r["tau_us"] for r in sweep], max(b))
+    L = wl.ctx_lens.astype(np.int64)
+    T = binding.replica_time(tau, L)
+    sh = binding.request_shares(tau, L)
+    top = np.argsort(L)[::-1][:max(1, len(L) // 20)]
+    return dict(tau_source="sweep mean tau_us per batch size", bmax=max(b),
+                bulk_requests=len(L), bulk_replica_attention_s=round(T / 1e6, 6),
+                longest_5pct_share=round(float(sh[top].sum() / T), 4))
+
+
 def sweep_summary(points):
     """Per batch size: mean, min and max over seeds of the sweep figures."""
     out = []
@@ -237,9 +254,11 @@ def main():
             tail[name]["kernel_frac"] = round(r["kernel_gbps"] / PEAK_GBPS, 4)
             tail[name]["traffic"] = measured_traffic(name)
     sweep = []
+    model = None
     if not args.no_sweep:
         log(f"[bench] concurrency sweep ({args.sweep_seeds} seeds)")
         sweep = sweep_summary(binding.concurrency_sweep(seeds=args.sweep_seeds, warmup=20, iters=30))
+        model = makespan_model(sweep, bulk["wl"])
     cpu = None if args.no_cpu_baseline else cpu_baseline(bulk["wl"])
 
     achieved = bulk["kernel_gbps"]
@@ -270,6 +289,7 @@ def main():
         "cpu_baseline": cpu,
         "tail": tail,
         "sweep": sweep,
+        "makespan_model": model,
     }
     print(json.dumps(line), flush=True)
 

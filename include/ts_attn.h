@@ -177,6 +177,41 @@ typedef struct ts_sweep_point {
 int ts_concurrency_sweep(const ts_sweep_config *cfg, ts_sweep_point *pts, int32_t cap,
                          int32_t *n_out);
 
+/* ---- replica completion-time model ------------------------------------------
+ * Host-only (no GPU needed).  The paper turns the measured per-token decoding
+ * time tau(b) = 1 / v(b) at active batch b (Sec. 2.1) into rollout time under
+ * the all-admit model: a replica serving requests of completion lengths L_i
+ * decodes position x with b(x) = #{i : L_i >= x} requests active, at cost
+ * tau(b(x)).  Its completion time is
+ *     T = sum_x tau(b(x)) = sum_j tau(j) (L_j - L_{j+1})   (L sorted descending)
+ * (Sec. 2.1; App. D), request i's share of it is sum_{x <= L_i} tau(b(x)) /
+ * b(x) (App. D; the shares add up to T), and a rollout step's makespan is the
+ * largest T over the replicas (App. D).  `tau` arrays are dense tables with
+ * tau[b - 1] = tau(b) for b = 1 .. bmax, in any time unit (results are in the
+ * same unit); lengths are tokens (>= 0).  All entry points return TS_OK or a
+ * negative ts_status with ts_last_error() set, and write nothing on error. */
+
+/* Dense table tau_dense[b - 1], b = 1 .. bmax, from m measured points
+ * (batch[k], tau[k]) with strictly increasing batch sizes >= 1: linear between
+ * points, the first value below the first point, linear extrapolation of the
+ * last segment past the last point (clamped at 0). */
+int ts_tau_table(const int32_t *batch, const double *tau, int32_t m, int32_t bmax, double *tau_dense);
+
+/* Completion time of one replica holding n requests (n <= bmax). */
+int ts_replica_time(const double *tau, int32_t bmax, const int64_t *lengths, int32_t n, double *T);
+
+/* Each request's share of its replica's completion time (shares[i] for
+ * lengths[i]; equal lengths get equal shares). */
+int ts_request_shares(const double *tau, int32_t bmax, const int64_t *lengths, int32_t n,
+                      double *shares);
+
+/* Rollout-step makespan of an assignment: request i runs on replica
+ * replica[i] in [0, n_replicas); writes each replica's completion time to
+ * T_replica[r] and their maximum to *T_step.  Each replica may hold at most
+ * bmax requests. */
+int ts_step_makespan(const double *tau, int32_t bmax, const int64_t *lengths, const int32_t *replica,
+                     int32_t n, int32_t n_replicas, double *T_replica, double *T_step);
+
 /* ---- synthetic inputs (same definitions as the test generator) -------------
  * SplitMix64 (Steele, Lea, Flood 2014) addressed by (seed, stream, index):
  * value n = mix64(mix64((seed << 8) + stream) + (n + 1) * 0x9E3779B97F4A7C15);

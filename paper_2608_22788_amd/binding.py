@@ -56,7 +56,7 @@ EXPORTS = ["ts_decode_attn_workspace_size", "ts_decode_attn", "ts_decode_attn_ev
            "ts_concurrency_sweep", "ts_synth_fill_bf16", "ts_synth_sweep_lengths",
            "ts_synth_page_table", "ts_copy_bytes", "ts_stream_read", "ts_event_create", "ts_event_destroy",
            "ts_event_record", "ts_event_elapsed_ms", "ts_status_string", "ts_last_error",
-           "ts_version"]
+           "ts_version", "ts_tau_table", "ts_replica_time", "ts_request_shares", "ts_step_makespan"]
 
 
 def _load() -> ctypes.CDLL:
@@ -100,6 +100,14 @@ def _load() -> ctypes.CDLL:
     lib.ts_event_record.restype = ctypes.c_int
     lib.ts_event_elapsed_ms.argtypes = [P, P, ctypes.POINTER(ctypes.c_float)]
     lib.ts_event_elapsed_ms.restype = ctypes.c_int
+    lib.ts_tau_table.argtypes = [P, P, I32, I32, P]
+    lib.ts_tau_table.restype = ctypes.c_int
+    lib.ts_replica_time.argtypes = [P, I32, P, I32, ctypes.POINTER(ctypes.c_double)]
+    lib.ts_replica_time.restype = ctypes.c_int
+    lib.ts_request_shares.argtypes = [P, I32, P, I32, P]
+    lib.ts_request_shares.restype = ctypes.c_int
+    lib.ts_step_makespan.argtypes = [P, I32, P, P, I32, I32, P, ctypes.POINTER(ctypes.c_double)]
+    lib.ts_step_makespan.restype = ctypes.c_int
     lib.ts_status_string.argtypes = [ctypes.c_int]
     lib.ts_status_string.restype = ctypes.c_char_p
     lib.ts_last_error.argtypes = []
@@ -275,3 +283,53 @@ def concurrency_sweep(batches: Sequence[int] = (1, 2, 4, 8, 16, 32, 64, 128, 256
     n = ctypes.c_int32()
     check(lib.ts_concurrency_sweep(ctypes.byref(cfg), pts, cap, ctypes.byref(n)), "ts_concurrency_sweep")
     return [{f: getattr(pts[i], f) for f, _ in SweepPoint._fields_} for i in range(n.value)]
+
+
+# ---- replica completion-time model (host only) ------------------------------
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _i64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+def tau_table(batch: Sequence[int], tau: Sequence[float], bmax: int) -> np.ndarray:
+    """Dense tau(b), b = 1..bmax, from measured (batch, tau) points."""
+    b = np.ascontiguousarray(batch, dtype=np.int32)
+    t = _f64(tau)
+    if b.shape != t.shape:
+        raise ValueError("batch and tau differ in length")
+    out = np.empty(bmax, dtype=np.float64)
+    check(lib.ts_tau_table(b.ctypes.data, t.ctypes.data, len(b), bmax, out.ctypes.data), "ts_tau_table")
+    return out
+
+
+def replica_time(tau: Sequence[float], lengths: Sequence[int]) -> float:
+    t, L = _f64(tau), _i64(lengths)
+    T = ctypes.c_double()
+    check(lib.ts_replica_time(t.ctypes.data, len(t), L.ctypes.data, len(L), ctypes.byref(T)),
+          "ts_replica_time")
+    return T.value
+
+
+def request_shares(tau: Sequence[float], lengths: Sequence[int]) -> np.ndarray:
+    t, L = _f64(tau), _i64(lengths)
+    out = np.empty(len(L), dtype=np.float64)
+    check(lib.ts_request_shares(t.ctypes.data, len(t), L.ctypes.data, len(L), out.ctypes.data),
+          "ts_request_shares")
+    return out
+
+
+def step_makespan(tau: Sequence[float], lengths: Sequence[int], replica: Sequence[int], n_replicas: int):
+    """(completion time per replica, step makespan)."""
+    t, L = _f64(tau), _i64(lengths)
+    r = np.ascontiguousarray(replica, dtype=np.int32)
+    if len(r) != len(L):
+        raise ValueError("lengths and replica differ in length")
+    times = np.empty(max(n_replicas, 0), dtype=np.float64)
+    T = ctypes.c_double()
+    check(lib.ts_step_makespan(t.ctypes.data, len(t), L.ctypes.data, r.ctypes.data, len(L), n_replicas,
+                               times.ctypes.data, ctypes.byref(T)), "ts_step_makespan")
+    return times, T.value

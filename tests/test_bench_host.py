@@ -47,3 +47,26 @@ def test_traffic_counts_only_for_matching_sources(bench, tmp_path, monkeypatch):
     assert bench.measured_traffic("mtp") is None        # stale: sources changed since
     assert bench.measured_traffic("bulk") is None       # never measured
     assert len(h) == 16 and h != bench.kernel_hash("bulk")
+
+
+def test_makespan_model_block(bench):
+    """The bench's model block: the replica time of the bulk lengths under a
+    tau curve equals the position-by-position oracle on the same table."""
+    import numpy as np
+    from oracle import makespan as om
+    from paper_2608_22788_amd import binding, synth
+    wl = synth.make_workload("bulk", seed=0)
+    pts = [(1, 4.6), (2, 5.0), (4, 5.6), (8, 7.1), (16, 53.0), (32, 88.0), (64, 153.0), (128, 288.0),
+           (256, 554.0), (512, 1066.0)]
+    sweep = [dict(batch=b, tau_us=t) for b, t in pts]
+    out = bench.makespan_model(sweep, wl)
+    tau = binding.tau_table([b for b, _ in pts], [t for _, t in pts], 512)
+    L = wl.ctx_lens.astype(np.int64)
+    s = sorted(L.tolist(), reverse=True) + [0]
+    closed = sum(tau[j] * (s[j] - s[j + 1]) for j in range(len(L)))
+    assert out["bulk_replica_attention_s"] == round(closed / 1e6, 6)
+    assert out["bulk_requests"] == 256 and 0.05 < out["longest_5pct_share"] < 1.0
+    # the shares of a few requests, position by position
+    small = L[:12].tolist()
+    np.testing.assert_allclose(binding.request_shares(tau, small), om.request_shares(tau.tolist(), small),
+                               rtol=1e-12)
