@@ -37,11 +37,11 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.md")
 # launch; a traffic figure counts only while their hash matches the one it was
 # measured on.
 TRAFFIC_SOURCES = {
-    "bulk": ["csrc/attn_common.h", "csrc/attn_split.h", "csrc/attn_decode.hip", "csrc/api.hip", "build.py"],
-    "mtp": ["csrc/attn_common.h", "csrc/attn_verify.hip", "csrc/api.hip", "build.py"],
+    "bulk": ["csrc/attn_common.h", "csrc/attn_split.h", "csrc/attn_verify.hip", "csrc/api.hip", "build.py"],
+    "mtp": ["csrc/attn_common.h", "csrc/attn_split.h", "csrc/attn_verify.hip", "csrc/api.hip", "build.py"],
     "dflash": ["csrc/attn_common.h", "csrc/attn_verify_team.hip", "csrc/api.hip", "build.py"],
 }
-KERNELS = {"bulk": "decode_q1_kernel<128,4>", "mtp": "verify_kernel<128,1>",
+KERNELS = {"bulk": "verify_kernel<128,1>", "mtp": "verify_kernel<128,1>",
            "dflash": "verify_team_kernel<4>"}
 
 WORKLOADS = {
@@ -190,6 +190,22 @@ def makespan_model(sweep, wl):
                 longest_5pct_share=round(float(sh[top].sum() / T), 4))
 
 
+def depth_sweep(depths=(1, 2, 3, 4, 5, 6), seed_count=1):
+    """Route-specialised speculative decoding (Sec. 3.4, Sec. 4.3): the same
+    concurrency sweep with every batch size verifying q_len = 1 + gamma
+    tokens per sequence.  tau_us (call time / q_len) is the attention time per
+    drafted position if every draft is accepted."""
+    from paper_2608_22788_amd import binding
+    rows = []
+    for q in depths:
+        pts = binding.concurrency_sweep(seeds=seed_count, warmup=10, iters=20, verify_max_batch=4096,
+                                        verify_q_len=q)
+        for r in sweep_summary(pts):
+            rows.append(dict(q_len=q, batch=r["batch"], kv_gbps=r["kv_gbps"], call_us=round(r["tau_us"] * q, 2),
+                             tau_us=r["tau_us"]))
+    return rows
+
+
 def sweep_summary(points):
     """Per batch size: mean, min and max over seeds of the sweep figures."""
     out = []
@@ -214,6 +230,7 @@ def main():
     ap.add_argument("--no-tail", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--sweep-seeds", type=int, default=5)
+    ap.add_argument("--no-depth-sweep", action="store_true")
     ap.add_argument("--only", choices=list(WORKLOADS), help="time one workload only (profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="with --only: first copy BYTES with the library's plain copy kernel, "
@@ -259,6 +276,10 @@ def main():
         log(f"[bench] concurrency sweep ({args.sweep_seeds} seeds)")
         sweep = sweep_summary(binding.concurrency_sweep(seeds=args.sweep_seeds, warmup=20, iters=30))
         model = makespan_model(sweep, bulk["wl"])
+    depth = None
+    if not args.no_depth_sweep:
+        log("[bench] draft-depth sweep (q_len 1..6 at every batch size, seed 0)")
+        depth = depth_sweep()
     cpu = None if args.no_cpu_baseline else cpu_baseline(bulk["wl"])
 
     achieved = bulk["kernel_gbps"]
@@ -290,6 +311,7 @@ def main():
         "tail": tail,
         "sweep": sweep,
         "makespan_model": model,
+        "depth_sweep": depth,
     }
     print(json.dumps(line), flush=True)
 

@@ -83,14 +83,20 @@ typedef enum ts_status {
  * wavefront, or a four-wavefront team for verify at head_dim 128) share the
  * KV stream; a positive value fixes it (the result does not depend on it
  * beyond rounding; tests use it to vary the split points).  variant selects
- * the kernel for max_q_len > 1: TS_VARIANT_AUTO, TS_VARIANT_WAVE (one
- * wavefront holds every row block) or TS_VARIANT_TEAM (head_dim 128 only:
- * four wavefronts share each page through LDS); it is ignored for
- * max_q_len == 1 with a group size of 1, 2, 4 or 8, which always uses the
- * one-token decode kernel. */
+ * the kernel:
+ *   TS_VARIANT_AUTO  the matrix-core kernel in which one wavefront holds
+ *                    every row block for up to 32 rows per (sequence, KV
+ *                    head), the team kernel beyond (head_dim 128);
+ *   TS_VARIANT_WAVE  the single-wavefront matrix-core kernel, any shape;
+ *   TS_VARIANT_TEAM  head_dim 128 only: four wavefronts share each page
+ *                    through LDS;
+ *   TS_VARIANT_VALU  max_q_len 1 with a group size of 1, 2, 4 or 8 only: the
+ *                    one-token kernel on vector ALUs (dot2), kept for
+ *                    comparison; the matrix-core kernel measured faster. */
 #define TS_VARIANT_AUTO 0
 #define TS_VARIANT_WAVE 1
 #define TS_VARIANT_TEAM 2
+#define TS_VARIANT_VALU 3
 
 typedef struct ts_attn_shape {
     int32_t num_seqs;

@@ -31,7 +31,7 @@ class AttnShape(ctypes.Structure):
                 ("variant", ctypes.c_int32)]
 
 
-VARIANT_AUTO, VARIANT_WAVE, VARIANT_TEAM = 0, 1, 2
+VARIANT_AUTO, VARIANT_WAVE, VARIANT_TEAM, VARIANT_VALU = 0, 1, 2, 3
 
 
 class SweepConfig(ctypes.Structure):

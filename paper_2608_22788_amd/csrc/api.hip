@@ -79,21 +79,24 @@ struct Plan {
 
 // Number of workers sharing the KV stream.  MI355X has 256 compute units.
 // Measured (after a clock warm-up of a few hundred calls) on the bulk, MTP and
-// block-draft workloads: the decode kernel is best with 4 single-wavefront
-// workers per compute unit (1024), the single-wavefront verify kernel with 3
-// (768; 1024 is within 1 %), and the team verify kernel with 2 teams per
-// compute unit (512), although its registers would allow 3: the third team
-// lowers throughput by 8 %.  The auto count is further capped at launch by
+// block-draft workloads: the VALU decode kernel is best with 4 wavefronts per
+// compute unit (1024); the single-wavefront matrix-core kernel with 4 for up
+// to 8 rows per unit (one-token decode; at head_dim 64 the 4th is worth 7 %)
+// and with 3 for more (768 on the MTP workload; 1024 is within 1 %); the
+// team kernel with 2 teams per compute unit (512), although its registers
+// would allow 3: the third team lowers throughput by 8 %.  The auto count is further capped at launch by
 // the occupancy the HIP runtime reports for the compiled kernel, so all
 // workers run in one round.
-static int per_cu_bound(bool q1, bool team) {
+static int per_cu_bound(bool q1, bool team, int rows) {
     if (q1)
         return 4;
-    return team ? 2 : 3;
+    if (team)
+        return 2;
+    return rows <= 8 ? 4 : 3;
 }
 
-static int auto_workers(const ts_attn_shape *s, bool q1, bool team) {
-    int64_t w = 256LL * per_cu_bound(q1, team);
+static int auto_workers(const ts_attn_shape *s, bool q1, bool team, int rows) {
+    int64_t w = 256LL * per_cu_bound(q1, team, rows);
     // Small shapes get fewer workers so that each has at least a few pages.
     const int64_t pages_ub = (int64_t)s->num_seqs * s->num_kv_heads *
                              ((s->max_ctx_len + kPage - 1) / kPage);
@@ -161,21 +164,28 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
         return fail(TS_ERR_SHAPE, "num_pages %lld outside [1, 2^31]", (long long)s->num_pages);
     if (s->num_workers < 0 || s->num_workers > (1 << 20))
         return fail(TS_ERR_SHAPE, "num_workers %d outside [0, 2^20]", s->num_workers);
-    if (s->variant < TS_VARIANT_AUTO || s->variant > TS_VARIANT_TEAM)
+    if (s->variant < TS_VARIANT_AUTO || s->variant > TS_VARIANT_VALU)
         return fail(TS_ERR_SHAPE, "variant %d unknown", s->variant);
     if (s->variant == TS_VARIANT_TEAM && s->head_dim != 128)
         return fail(TS_ERR_SHAPE, "the team verify kernel needs head_dim 128");
 
     pl->G = G;
-    pl->q1 = (s->max_q_len == 1) && (G == 1 || G == 2 || G == 4 || G == 8);
+    // The one-token VALU kernel runs only on request: the single-wavefront
+    // matrix-core kernel was measured faster on one-token decode too (bulk
+    // workload 2.5 %, 16-128 sequences 5-14 %, group size 8 by 19 %).
+    pl->q1 = s->variant == TS_VARIANT_VALU;
+    if (pl->q1 && !(s->max_q_len == 1 && (G == 1 || G == 2 || G == 4 || G == 8)))
+        return fail(TS_ERR_SHAPE, "the VALU decode kernel needs max_q_len 1 and a group size of 1, 2, 4 or 8");
     pl->rows_per_unit = G * s->max_q_len;
     pl->NB = (pl->rows_per_unit + 15) / 16;
-    // One row block fits one wavefront's registers and runs best that way
-    // (measured on the MTP workload); more row blocks need the team kernel.
+    // Up to two row blocks (32 rows) run best on one wavefront (MTP workload;
+    // 20-24 rows at 4-512 sequences: 3-7 % ahead of the team kernel); from
+    // three row blocks on the team kernel, which shares each page through LDS
+    // (block-draft workload, 64 rows: 12 % ahead at 4 sequences).
     pl->team = !pl->q1 && s->head_dim == 128 &&
-               (s->variant == TS_VARIANT_TEAM || (s->variant == TS_VARIANT_AUTO && pl->NB >= 2));
+               (s->variant == TS_VARIANT_TEAM || (s->variant == TS_VARIANT_AUTO && pl->NB >= 3));
     pl->auto_w = s->num_workers == 0;
-    pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team);
+    pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team, pl->rows_per_unit);
     // Workspace: the split counters first, at a fixed size whatever the shape,
     // so that no call's partial results ever land on them; then the partial
     // outputs and their log-sum-exp.
@@ -276,9 +286,10 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
             pl.W = resident;
         p.W = pl.W;
     }
-    // The one-token kernel combines its splits itself when there are at least
-    // twice as many units as workers (a unit then has one or two pieces).
-    p.fuse_splits = pl.q1 && (int64_t)p.B * p.Hkv >= 2 * (int64_t)p.W;
+    // The single-wavefront kernels combine their splits themselves when there
+    // are at least twice as many units as workers (a unit then has one or two
+    // pieces); otherwise the merge kernel does.
+    p.fuse_splits = !pl.team && (int64_t)p.B * p.Hkv >= 2 * (int64_t)p.W;
 
     hipError_t e;
     if (ev_begin || ev_end) {

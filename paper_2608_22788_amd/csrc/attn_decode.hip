@@ -180,34 +180,6 @@ struct DecodeQ1 {
         }
     }
 
-    // The last worker to finish a piece of the unit combines all pieces.  The
-    // partials were written with device-coherent stores; once they are
-    // complete (vector memory counter drained) the arrival is counted, and
-    // the last arriver reads the others' partials with device-coherent loads
-    // issued after its count returned.
-    __device__ static void arrive(const AttnParams &p, const Segment &s, int64_t ptot, int lane) {
-        wait_vmem();
-        int *cnt = p.counters + (size_t)s.b * p.Hkv + s.g;
-        int old = 0;
-        if (lane == 0)
-            old = atomicAdd(cnt, 1);
-        old = first_lane_int(old);
-        const UnitSplit u = unit_split(ptot, s.us, s.np, p.W);
-        if (old != u.nparts - 1)
-            return;
-        const int part = lane & 15;
-#pragma unroll
-        for (int r0 = 0; r0 < G; r0 += 4) {
-            const int r = r0 + (lane >> 4);
-            Acc<D / 16> a;
-            a.init();
-            gather_partials<D, true>(p, u, r < G ? r : 0, part, 0, 1, a);
-            if (r < G)
-                write_merged<D>(p, s.b, s.g, r, part, a);
-        }
-        __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-
     __device__ static void segment(const AttnParams &p, const Segment &s, int slot_id, int64_t ptot) {
         const int lane = threadIdx.x;
         const int slot = lane >> 3;
@@ -333,7 +305,7 @@ struct DecodeQ1 {
             }
         }
         if (!s.whole && p.fuse_splits)
-            arrive(p, s, ptot, lane);
+            arrive_and_combine<D>(p, s, ptot, lane);
     }
 };
 

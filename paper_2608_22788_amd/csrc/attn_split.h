@@ -31,11 +31,13 @@ __device__ __forceinline__ void st_coherent(float *p, float v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 // 16-byte form of st_coherent (p 16-byte aligned).  The device-scope policy
-// bit is only reachable for vector stores through an instruction written out;
-// the data registers are read when the store issues, and wait_vmem() below
-// covers its completion.
+// bit is only reachable for vector stores through an instruction written out.
+// A store of more than 8 bytes still reads its data registers for a moment
+// after it issues, and the compiler does not see inside the instruction to
+// protect them (it reused them at once and corrupted partial rows), so two
+// wait states follow it.  wait_vmem() below covers the store's completion.
 __device__ __forceinline__ void st_coherent16(float *p, f32x4_t v) {
-    asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+    asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" : : "v"(p), "v"(v) : "memory");
 }
 // Waits until every vector memory operation this wavefront issued is complete.
 __device__ __forceinline__ void wait_vmem() {
@@ -177,6 +179,44 @@ __device__ __forceinline__ void write_merged(const AttnParams &p, int b, int g, 
         *reinterpret_cast<uint4 *>(dst) = make_uint4(w2[0], w2[1], w2[2], w2[3]);
     else
         *reinterpret_cast<uint2 *>(dst) = make_uint2(w2[0], w2[1]);
+}
+
+// Combines all pieces of unit (b, g) and writes its rows (one wavefront;
+// rows_per_unit rows, 4 per pass; rows of draft positions >= q_len are
+// skipped).  Called by the worker that counted the last arrival on the unit,
+// which then sets the counter back to zero for the next call.
+template <int D>
+__device__ void combine_unit(const AttnParams &p, int b, int g, const UnitSplit &u, int lane) {
+    const int part = lane & 15;
+    const int R = p.rows_per_unit;
+    const int Q = ld_meta(p.q_lens, b);
+    for (int r0 = 0; r0 < R; r0 += 4) {
+        const int r = r0 + (lane >> 4);
+        const bool row_ok = r < R && r / p.G < Q;
+        Acc<D / 16> a;
+        a.init();
+        gather_partials<D, true>(p, u, row_ok ? r : 0, part, 0, 1, a);
+        if (row_ok)
+            write_merged<D>(p, b, g, r, part, a);
+    }
+    __hip_atomic_store(p.counters + (size_t)b * p.Hkv + g, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Counts this wavefront's arrival on the unit of a piece whose partial it has
+// just written with device-coherent stores; the last arriver combines the
+// unit.  The stores are complete once the vector memory counter has drained,
+// so no cache-wide fence is needed, and the last arriver's loads are issued
+// after its count returned.
+template <int D>
+__device__ void arrive_and_combine(const AttnParams &p, const Segment &s, int64_t ptot, int lane) {
+    wait_vmem();
+    int old = 0;
+    if (lane == 0)
+        old = atomicAdd(p.counters + (size_t)s.b * p.Hkv + s.g, 1);
+    old = first_lane_int(old);
+    const UnitSplit u = unit_split(ptot, s.us, s.np, p.W);
+    if (old == u.nparts - 1)
+        combine_unit<D>(p, s.b, s.g, u, lane);
 }
 
 }  // namespace tsattn

@@ -29,7 +29,9 @@
 // Masks: key t is visible to draft row i iff t <= L - Q + i; keys past the
 // segment end or the context end get probability 0 and their value rows are
 // zeroed before the product, so stale data never reaches the output.
-#include "attn_common.h"
+// With p.fuse_splits the last worker to finish a piece of a unit combines the
+// unit's pieces itself (attn_split.h) instead of the merge kernel.
+#include "attn_split.h"
 
 namespace tsattn {
 
@@ -166,7 +168,7 @@ struct Verify {
         }
     }
 
-    __device__ static void segment(const AttnParams &p, const Segment &s, int slot_id) {
+    __device__ static void segment(const AttnParams &p, const Segment &s, int slot_id, int64_t ptot) {
         const int lane = threadIdx.x;
         const int n = lane & 15;
         const int kq = lane >> 4;
@@ -241,16 +243,29 @@ struct Verify {
                 } else {
                     const size_t row = (size_t)slot_id * R + r;
                     float *dst = p.ws_o + row * D + VE * n;
+                    const float lse = l > 0.0f ? m + __log2f(l) : -INFINITY;
+                    if (p.fuse_splits) {
+                        // device-coherent: the unit's last arriver combines it
 #pragma unroll
-                    for (int e = 0; e < VE; e += 4)
-                        *reinterpret_cast<float4 *>(dst + e) =
-                            make_float4(st.acc[rb][e][i] * inv, st.acc[rb][e + 1][i] * inv,
-                                        st.acc[rb][e + 2][i] * inv, st.acc[rb][e + 3][i] * inv);
-                    if (n == 0)
-                        p.ws_lse[row] = l > 0.0f ? m + __log2f(l) : -INFINITY;
+                        for (int e = 0; e < VE; e += 4)
+                            st_coherent16(dst + e, f32x4_t{st.acc[rb][e][i] * inv, st.acc[rb][e + 1][i] * inv,
+                                                           st.acc[rb][e + 2][i] * inv, st.acc[rb][e + 3][i] * inv});
+                        if (n == 0)
+                            st_coherent(p.ws_lse + row, lse);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < VE; e += 4)
+                            *reinterpret_cast<float4 *>(dst + e) =
+                                make_float4(st.acc[rb][e][i] * inv, st.acc[rb][e + 1][i] * inv,
+                                            st.acc[rb][e + 2][i] * inv, st.acc[rb][e + 3][i] * inv);
+                        if (n == 0)
+                            p.ws_lse[row] = lse;
+                    }
                 }
             }
         }
+        if (!s.whole && p.fuse_splits)
+            arrive_and_combine<D>(p, s, ptot, lane);
     }
 };
 
@@ -264,7 +279,7 @@ __global__ __launch_bounds__(64) void verify_kernel(AttnParams p) {
     const int64_t end = worker_begin(ptot, w + 1, p.W);
     for (int64_t x = begin; x < end;) {
         const Segment s = locate(p, s_pre, x, end);
-        Verify<D, NB>::segment(p, s, x == begin ? 2 * w : 2 * w + 1);
+        Verify<D, NB>::segment(p, s, x == begin ? 2 * w : 2 * w + 1, ptot);
         x = s.next;
     }
 }

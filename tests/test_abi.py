@@ -67,6 +67,12 @@ def test_variant_checks():
     assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) > 0
     s.variant = b.VARIANT_WAVE
     assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) > 0
+    s.variant = b.VARIANT_VALU          # the VALU kernel is one-token only
+    assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) == 0
+    s.max_q_len = 1
+    assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) > 0
+    s.variant = 4
+    assert b.lib.ts_decode_attn_workspace_size(ctypes.byref(s)) == 0
 
 
 def test_page_size_must_be_16():

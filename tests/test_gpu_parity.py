@@ -40,10 +40,13 @@ def test_device_fill_matches_host_generator(dev):
 
 
 def variants_for(wl):
-    """Kernel variants that apply to a workload (both verify kernels at d128)."""
-    if wl.Qmax > 1 and wl.D == 128:
-        return (1, 2)
-    return (0,)
+    """Kernel variants to check for a workload: the automatic choice, the
+    single-wavefront matrix-core kernel, at head_dim 128 the team kernel, and
+    for one-token decode with a group size of 1, 2, 4 or 8 the VALU kernel."""
+    v = [0, 1] + ([2] if wl.D == 128 else [])
+    if wl.Qmax == 1 and wl.Hq // wl.Hkv in (1, 2, 4, 8):
+        v.append(3)
+    return tuple(v)
 
 
 def run_case(dev, orc, wl, workers=(0,), values="host"):
@@ -133,7 +136,7 @@ def test_workspace_reused_across_calls_and_shapes(dev, orc):
 
 def test_one_key_returns_value_row_bitwise(dev, orc):
     _, device = dev
-    for Qmax, var in ((1, 0), (2, 1), (2, 2)):
+    for Qmax, var in ((1, 0), (1, 3), (2, 1), (2, 2)):
         wl = synth.make_workload("onekey", seed=9, cfg=small_cfg(32, 8, 128), ctx_lens=[1, 1, 1],
                                  q_lens=[1, 1, 1], Qmax=Qmax)
         t = device.upload(wl)
@@ -148,7 +151,7 @@ def test_one_key_returns_value_row_bitwise(dev, orc):
 def test_constant_values_give_exactly_that_value(dev):
     import torch
     _, device = dev
-    for q, var in ((1, 0), (4, 1), (4, 2), (16, 1), (16, 2)):
+    for q, var in ((1, 0), (1, 3), (4, 1), (4, 2), (16, 1), (16, 2)):
         wl = synth.make_workload("constv", seed=4, cfg=small_cfg(32, 8, 128), ctx_lens=[q + 40, 3000],
                                  q_lens=[q, q])
         t = device.upload(wl, values="device")
