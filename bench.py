@@ -206,6 +206,93 @@ def depth_sweep(depths=(1, 2, 3, 4, 5, 6), seed_count=1):
     return rows
 
 
+def mixed_and_graph(steps=50):
+    """Ragged mixed batches and graph capture (the engine-side problem the
+    paper cites for variable draft lengths, Sec. 3.4).  The bulk workload's
+    256 sequences where the 8 longest verify 4 tokens (MTP-3) and the rest
+    decode 1, timed as one launch (max_q_len 4, ragged q_lens) against the
+    same work as two launches (248 x q_len 1, 8 x q_len 4).  Then a small
+    ragged step (8 sequences of the sweep's lengths, q_lens 4,4,1,...)
+    captured once into a HIP graph and replayed, against eager calls from
+    Python."""
+    import torch
+    from paper_2608_22788_amd import binding, device, synth
+    base = synth.make_workload("bulk", seed=0)
+    tail = np.argsort(base.ctx_lens)[::-1][:8]
+    ql = np.ones(base.B, dtype=np.int64)
+    ql[tail] = 4
+    wl = synth.make_workload("bulk", seed=0, q_lens=ql.tolist(), Qmax=4)
+    t, pools = make_pools(wl, 2)
+    bulk_idx = torch.from_numpy(np.setdiff1d(np.arange(wl.B), tail)).cuda()
+    tail_idx = torch.from_numpy(np.sort(tail).copy()).cuda()
+    parts = []
+    for idx, q in ((bulk_idx, 1), (tail_idx, 4)):
+        parts.append(dict(q=t["q"][idx, :q].contiguous(), page_table=t["page_table"][idx].contiguous(),
+                          ctx_lens=t["ctx_lens"][idx].contiguous(), q_lens=t["q_lens"][idx].contiguous(),
+                          out=torch.empty_like(t["q"][idx, :q]).contiguous()))
+    ws = binding.new_workspace(256 << 20)
+
+    def one(i):
+        k, v = pools[i % 2]
+        binding.decode_attn(t["q"], k, v, t["page_table"], t["ctx_lens"], t["q_lens"], t["out"], wl.scale,
+                            workspace=ws, max_ctx_len=wl.max_ctx_len)
+
+    def two(i):
+        k, v = pools[i % 2]
+        for pt in parts:
+            binding.decode_attn(pt["q"], k, v, pt["page_table"], pt["ctx_lens"], pt["q_lens"], pt["out"],
+                                wl.scale, workspace=ws, max_ctx_len=wl.max_ctx_len)
+
+    def timed(fn):
+        for i in range(100):
+            fn(i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            fn(i)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / steps * 1e6
+
+    res = dict(workload="bulk lengths, 8 longest verify q_len 4, 248 decode q_len 1",
+               kv_bytes=wl.kv_bytes(), one_launch_us=round(timed(one), 2), two_launches_us=round(timed(two), 2))
+    res["one_launch_kv_gbps"] = round(wl.kv_bytes() / res["one_launch_us"] / 1e3, 1)
+    del pools, t, parts
+
+    # a small ragged step in a graph
+    sw = synth.make_workload("sweep_b8", seed=0, q_lens=[4, 4, 1, 1, 4, 1, 1, 1], Qmax=4)
+    n_pools = max(2, -(-(1 << 30) // sw.kv_bytes()))
+    t, pools = make_pools(sw, n_pools)
+    ws2 = binding.new_workspace(binding.workspace_size(
+        binding.shape_of(t["q"], t["k_pages"], t["page_table"], sw.max_ctx_len)))
+
+    def small(i):
+        k, v = pools[i % n_pools]
+        binding.decode_attn(t["q"], k, v, t["page_table"], t["ctx_lens"], t["q_lens"], t["out"], sw.scale,
+                            workspace=ws2, max_ctx_len=sw.max_ctx_len)
+
+    eager = timed(small)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for i in range(n_pools):
+                small(i)
+    torch.cuda.current_stream().wait_stream(s)
+    reps = max(1, 200 // n_pools)
+    g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        g.replay()
+    torch.cuda.synchronize()
+    graph = (time.perf_counter() - t0) / (reps * n_pools) * 1e6
+    res.update(graph_workload="8 sequences (sweep lengths), q_lens 4,4,1,1,4,1,1,1",
+               eager_python_us=round(eager, 2), graph_replay_us=round(graph, 2))
+    del pools, t, g
+    return res
+
+
 def sweep_summary(points):
     """Per batch size: mean, min and max over seeds of the sweep figures."""
     out = []
@@ -231,6 +318,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--sweep-seeds", type=int, default=5)
     ap.add_argument("--no-depth-sweep", action="store_true")
+    ap.add_argument("--no-mixed", action="store_true")
     ap.add_argument("--only", choices=list(WORKLOADS), help="time one workload only (profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="with --only: first copy BYTES with the library's plain copy kernel, "
@@ -276,6 +364,10 @@ def main():
         log(f"[bench] concurrency sweep ({args.sweep_seeds} seeds)")
         sweep = sweep_summary(binding.concurrency_sweep(seeds=args.sweep_seeds, warmup=20, iters=30))
         model = makespan_model(sweep, bulk["wl"])
+    mixed = None
+    if not args.no_mixed:
+        log("[bench] ragged mixed batch and graph replay")
+        mixed = mixed_and_graph()
     depth = None
     if not args.no_depth_sweep:
         log("[bench] draft-depth sweep (q_len 1..6 at every batch size, seed 0)")
@@ -311,6 +403,7 @@ def main():
         "tail": tail,
         "sweep": sweep,
         "makespan_model": model,
+        "mixed_batch": mixed,
         "depth_sweep": depth,
     }
     print(json.dumps(line), flush=True)

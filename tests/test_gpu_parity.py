@@ -253,6 +253,28 @@ def test_full_size_config(dev, orc, name):
         assert_parity(got[seqs], ref, f"{name} seqs {seqs} variant {var}")
 
 
+def test_full_size_ragged_mixed_batch(dev, orc):
+    """One launch over the bulk workload in which the 8 longest sequences
+    verify 4 drafted tokens and the other 248 decode one (ragged q_lens under
+    max_q_len 4), the benchmark's mixed-batch case; sampled rows of both kinds
+    against the oracle, padded rows untouched."""
+    _, device = dev
+    base = synth.make_workload("bulk", seed=0)
+    tail = np.argsort(base.ctx_lens)[::-1][:8]
+    ql = np.ones(base.B, dtype=np.int64)
+    ql[tail] = 4
+    wl = synth.make_workload("bulk", seed=0, q_lens=ql.tolist(), Qmax=4)
+    t = device.upload(wl, values="device")
+    seqs = sorted(set(sample_seqs(wl, 4)) | {int(tail[0]), int(tail[5])})
+    ref = oracle_out(orc, wl.subset(seqs))
+    for var in variants_for(wl):
+        t["out_full"].fill_(device.CANARY)
+        device.run(wl, t, variant=var)
+        got = device.out_as_f64(t)
+        canary_ok(t, wl)
+        assert_parity(got[seqs], ref, f"mixed seqs {seqs} variant {var}")
+
+
 SWEEP_CASES = [(b, 0) for b in synth.SWEEP_BATCHES] + \
               [(b, s) for b in synth.SWEEP_BATCHES if b <= 64 for s in range(1, 5)]
 
