@@ -293,6 +293,75 @@ def mixed_and_graph(steps=50):
     return res
 
 
+def spec_step(steps=50, vocab=151936):
+    """One speculative verify step on the MTP and block-draft workloads
+    (Sec. 3.4): the KV append of the 1 + gamma new tokens, the verify
+    attention, and the lossless acceptance over a 151,936-token vocabulary
+    (synthetic fp32 distributions; the drafter's are the target's logits
+    plus noise, which accepts about half of the drafts).  Times each kernel
+    group alone and the three back to back."""
+    import torch
+    from paper_2608_22788_amd import binding, synth
+    out = {}
+    for name in ("mtp", "dflash"):
+        wl = synth.make_workload(name, seed=0)
+        t, pools = make_pools(wl, 2)
+        B, Q, G = wl.B, wl.Qmax, wl.Qmax - 1
+        gen = torch.Generator(device="cuda").manual_seed(1)
+        logits = torch.randn((B, Q, vocab), device="cuda", generator=gen) * 2.0
+        p = torch.softmax(logits, -1).contiguous()
+        q = torch.softmax(logits[:, :G] + 0.7 * torch.randn((B, G, vocab), device="cuda", generator=gen),
+                          -1).contiguous()
+        d = torch.multinomial(q.reshape(-1, vocab), 1, generator=gen).reshape(B, G).to(torch.int32)
+        nd = torch.full((B,), G, dtype=torch.int32, device="cuda")
+        ua = torch.rand((B, G), device="cuda", generator=gen)
+        us = torch.rand((B,), device="cuda", generator=gen)
+        na = torch.empty(B, dtype=torch.int32, device="cuda")
+        nt = torch.empty(B, dtype=torch.int32, device="cuda")
+        kn = torch.randn((B, Q, wl.Hkv, wl.D), device="cuda", generator=gen).to(torch.bfloat16)
+        vn = torch.randn((B, Q, wl.Hkv, wl.D), device="cuda", generator=gen).to(torch.bfloat16)
+        ws = binding.new_workspace(256 << 20)
+        aws = torch.empty(binding.lib.ts_spec_accept_workspace_size(B, vocab), dtype=torch.uint8, device="cuda")
+
+        def append(i):
+            k, v = pools[i % 2]
+            binding.kv_append(kn, vn, k, v, t["page_table"], t["ctx_lens"], t["q_lens"])
+
+        def attend(i):
+            k, v = pools[i % 2]
+            binding.decode_attn(t["q"], k, v, t["page_table"], t["ctx_lens"], t["q_lens"], t["out"], wl.scale,
+                                workspace=ws, max_ctx_len=wl.max_ctx_len)
+
+        def accept(i):
+            binding.spec_accept(p, q, d, nd, ua, us, na, nt, workspace=aws)
+
+        def step(i):
+            append(i)
+            attend(i)
+            accept(i)
+
+        def timed(fn):
+            for i in range(50):
+                fn(i)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(steps):
+                fn(i)
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t0) / steps * 1e6
+
+        r = {k: round(timed(fn), 2) for k, fn in (("append_us", append), ("attention_us", attend),
+                                                    ("accept_us", accept), ("step_us", step))}
+        acc = na.cpu().numpy()
+        rejected = int((acc < G).sum())
+        accept_bytes = (B + rejected) * vocab * 4
+        r.update(batch=B, q_len=Q, vocab=vocab, mean_accepted=round(float(acc.mean()), 2),
+                 accept_read_bytes=accept_bytes, accept_gbps=round(accept_bytes / r["accept_us"] / 1e3, 1))
+        out[name] = r
+        del pools, t, p, q, logits
+    return out
+
+
 def sweep_summary(points):
     """Per batch size: mean, min and max over seeds of the sweep figures."""
     out = []
@@ -319,6 +388,7 @@ def main():
     ap.add_argument("--sweep-seeds", type=int, default=5)
     ap.add_argument("--no-depth-sweep", action="store_true")
     ap.add_argument("--no-mixed", action="store_true")
+    ap.add_argument("--no-spec-step", action="store_true")
     ap.add_argument("--only", choices=list(WORKLOADS), help="time one workload only (profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="with --only: first copy BYTES with the library's plain copy kernel, "
@@ -368,6 +438,10 @@ def main():
     if not args.no_mixed:
         log("[bench] ragged mixed batch and graph replay")
         mixed = mixed_and_graph()
+    spec = None
+    if not args.no_spec_step:
+        log("[bench] speculative verify step: KV append, attention, acceptance")
+        spec = spec_step()
     depth = None
     if not args.no_depth_sweep:
         log("[bench] draft-depth sweep (q_len 1..6 at every batch size, seed 0)")
@@ -404,6 +478,7 @@ def main():
         "sweep": sweep,
         "makespan_model": model,
         "mixed_batch": mixed,
+        "spec_step": spec,
         "depth_sweep": depth,
     }
     print(json.dumps(line), flush=True)

@@ -183,6 +183,50 @@ typedef struct ts_sweep_point {
 int ts_concurrency_sweep(const ts_sweep_config *cfg, ts_sweep_point *pts, int32_t cap,
                          int32_t *n_out);
 
+/* ---- the steps around the verify attention ----------------------------------
+ * One speculative decoding step (Sec. 3.4: drafts are verified by the target
+ * model without changing its output distribution) writes the 1 + gamma new
+ * tokens' keys and values into the paged cache, runs ts_decode_attn over
+ * them, and after the model's remaining layers decides which drafts to keep.
+ * Both entry points are asynchronous on `stream`, allocate nothing and read
+ * no device data on the host. */
+
+/* KV append: for every sequence b and row i < q_lens[b] (token position
+ * t = ctx_lens[b] - q_lens[b] + i, i.e. ctx_lens already counts the new
+ * tokens), every KV head g:
+ *   k_pages[page_table[b][t / 16]][g][t % 16][:] = k_new[b][i][g][:]  (v alike)
+ * k_new, v_new: bf16 [num_seqs][max_q_len][num_kv_heads][head_dim], 16-byte
+ * aligned.  Uses num_seqs, num_kv_heads, head_dim (64 or 128), page_size (16),
+ * max_q_len, max_pages_per_seq and num_pages of the shape.  A row whose
+ * position or page id falls outside the pool is skipped, not written. */
+int ts_kv_append(const ts_attn_shape *shape, const void *k_new, const void *v_new, void *k_pages,
+                 void *v_pages, const int32_t *page_table, const int32_t *ctx_lens,
+                 const int32_t *q_lens, void *stream);
+
+/* Bytes of device workspace ts_spec_accept needs (256-byte aligned). */
+size_t ts_spec_accept_workspace_size(int32_t num_seqs, int32_t vocab);
+
+/* Lossless acceptance (speculative sampling, Leviathan et al. 2023, which
+ * the paper follows).  Sequence b proposed gamma_b = num_draft[b] (<=
+ * max_draft) tokens d_i = draft_tokens[b][i] drawn from the drafter's
+ * distributions q_draft[b][i][:]; the verify pass gave the target's
+ * distributions p_target[b][i][:] for i = 0 .. gamma_b (row gamma_b follows
+ * the last draft).  Draft i is accepted while u_accept[b][i] * q <= p (fp32;
+ * a draft id outside [0, vocab) is rejected); at the first rejection k the
+ * next token is drawn from max(0, p_k - q_k) (from p_k if that is all zero),
+ * after full acceptance from p_gamma, as the smallest token whose cumulative
+ * mass exceeds u_sample[b] times the total.  Writes num_accepted[b] (0 ..
+ * gamma_b) and next_token[b].
+ *   p_target  fp32 [num_seqs][max_draft + 1][vocab], 16-byte aligned
+ *   q_draft   fp32 [num_seqs][max_draft][vocab] (may be NULL if max_draft 0)
+ *   draft_tokens, u_accept  [num_seqs][max_draft];  num_draft, u_sample,
+ *   num_accepted, next_token  [num_seqs]; uniforms in [0, 1).
+ * The caller supplies the random numbers, so results are reproducible. */
+int ts_spec_accept(int32_t num_seqs, int32_t vocab, int32_t max_draft, const float *p_target,
+                   const float *q_draft, const int32_t *draft_tokens, const int32_t *num_draft,
+                   const float *u_accept, const float *u_sample, int32_t *num_accepted,
+                   int32_t *next_token, void *workspace, size_t workspace_bytes, void *stream);
+
 /* ---- replica completion-time model ------------------------------------------
  * Host-only (no GPU needed).  The paper turns the measured per-token decoding
  * time tau(b) = 1 / v(b) at active batch b (Sec. 2.1) into rollout time under

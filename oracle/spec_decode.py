@@ -85,7 +85,7 @@ def sample_inverse_cdf(weights: np.ndarray, u: float, tol: float = 1e-5) -> Tupl
     return v, near
 
 
-def spec_accept(p_target, q_draft, draft_tokens, num_draft, u_accept, u_sample):
+def spec_accept(p_target, q_draft, draft_tokens, num_draft, u_accept, u_sample, tol=1e-5):
     """Per sequence: (accepted draft count, next token, decision near a
     boundary).  p_target [B][Gmax+1][V], q_draft [B][Gmax][V] (float32
     probabilities), draft_tokens [B][Gmax], num_draft [B], u_accept [B][Gmax],
@@ -104,5 +104,5 @@ def spec_accept(p_target, q_draft, draft_tokens, num_draft, u_accept, u_sample):
                 w = p_target[b, k].astype(np.float64)
         else:
             w = p_target[b, g].astype(np.float64)
-        nxt[b], near[b] = sample_inverse_cdf(w, float(u_sample[b]))
+        nxt[b], near[b] = sample_inverse_cdf(w, float(u_sample[b]), tol)
     return n_acc, nxt, near

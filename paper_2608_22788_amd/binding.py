@@ -56,7 +56,8 @@ EXPORTS = ["ts_decode_attn_workspace_size", "ts_decode_attn", "ts_decode_attn_ev
            "ts_concurrency_sweep", "ts_synth_fill_bf16", "ts_synth_sweep_lengths",
            "ts_synth_page_table", "ts_copy_bytes", "ts_stream_read", "ts_event_create", "ts_event_destroy",
            "ts_event_record", "ts_event_elapsed_ms", "ts_status_string", "ts_last_error",
-           "ts_version", "ts_tau_table", "ts_replica_time", "ts_request_shares", "ts_step_makespan"]
+           "ts_version", "ts_tau_table", "ts_replica_time", "ts_request_shares", "ts_step_makespan",
+           "ts_kv_append", "ts_spec_accept_workspace_size", "ts_spec_accept"]
 
 
 def _load() -> ctypes.CDLL:
@@ -108,6 +109,12 @@ def _load() -> ctypes.CDLL:
     lib.ts_request_shares.restype = ctypes.c_int
     lib.ts_step_makespan.argtypes = [P, I32, P, P, I32, I32, P, ctypes.POINTER(ctypes.c_double)]
     lib.ts_step_makespan.restype = ctypes.c_int
+    lib.ts_kv_append.argtypes = [pshape, P, P, P, P, P, P, P, P]
+    lib.ts_kv_append.restype = ctypes.c_int
+    lib.ts_spec_accept_workspace_size.argtypes = [I32, I32]
+    lib.ts_spec_accept_workspace_size.restype = SZ
+    lib.ts_spec_accept.argtypes = [I32, I32, I32, P, P, P, P, P, P, P, P, P, SZ, P]
+    lib.ts_spec_accept.restype = ctypes.c_int
     lib.ts_status_string.argtypes = [ctypes.c_int]
     lib.ts_status_string.restype = ctypes.c_char_p
     lib.ts_last_error.argtypes = []
@@ -333,3 +340,36 @@ def step_makespan(tau: Sequence[float], lengths: Sequence[int], replica: Sequenc
     check(lib.ts_step_makespan(t.ctypes.data, len(t), L.ctypes.data, r.ctypes.data, len(L), n_replicas,
                                times.ctypes.data, ctypes.byref(T)), "ts_step_makespan")
     return times, T.value
+
+
+# ---- steps around the verify attention ----------------------------------------
+
+def kv_append(k_new, v_new, k_pages, v_pages, page_table, ctx_lens, q_lens, stream=None) -> None:
+    """ts_kv_append on torch tensors (k_new, v_new: bf16 [B][Qmax][Hkv][D])."""
+    B, Qmax, Hkv, D = k_new.shape
+    NP = k_pages.shape[0]
+    shape = make_shape(B, Hkv, Hkv, D, Qmax, page_table.shape[1], page_table.shape[1] * 16, NP)
+    for t in (k_new, v_new, k_pages, v_pages, page_table, ctx_lens, q_lens):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("kv_append needs contiguous CUDA tensors")
+    check(lib.ts_kv_append(ctypes.byref(shape), k_new.data_ptr(), v_new.data_ptr(), k_pages.data_ptr(),
+                           v_pages.data_ptr(), page_table.data_ptr(), ctx_lens.data_ptr(), q_lens.data_ptr(),
+                           _stream_ptr(stream)), "ts_kv_append")
+
+
+def spec_accept(p_target, q_draft, draft_tokens, num_draft, u_accept, u_sample, num_accepted, next_token,
+                workspace=None, stream=None):
+    """ts_spec_accept on torch tensors; returns the workspace used."""
+    import torch
+    B, G1, V = p_target.shape
+    G = G1 - 1
+    need = int(lib.ts_spec_accept_workspace_size(B, V))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=p_target.device)
+    ptr = lambda t: t.data_ptr() if t is not None else None  # noqa: E731
+    check(lib.ts_spec_accept(B, V, G, p_target.data_ptr(), ptr(q_draft), ptr(draft_tokens),
+                             num_draft.data_ptr(), ptr(u_accept), u_sample.data_ptr(), num_accepted.data_ptr(),
+                             next_token.data_ptr(), workspace.data_ptr(),
+                             workspace.numel() * workspace.element_size(), _stream_ptr(stream)),
+          "ts_spec_accept")
+    return workspace
