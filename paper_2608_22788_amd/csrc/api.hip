@@ -306,7 +306,7 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
     if ((e = hipGetLastError()) != hipSuccess)
         return hip_fail(e, "attention kernel launch");
     if (p.fuse_splits)
-        return TS_OK;   // the decode kernel combined its own splits
+        return TS_OK;   // the kernel combined its own splits
     const int ngroups = (pl.rows_per_unit + 3) / 4;
     const unsigned merge_blocks = (unsigned)(p.B * p.Hkv * ngroups);
     hipLaunchKernelGGL(merge_k, dim3(merge_blocks), dim3(4 * kWave), lds, hs, p);

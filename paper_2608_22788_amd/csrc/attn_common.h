@@ -47,7 +47,7 @@ struct AttnParams {
     int G;                      // Hq / Hkv
     int rows_per_unit;          // G * Qmax
     int W;                      // workers (wavefronts)
-    int fuse_splits;            // one-token kernel: combine splits in the kernel
+    int fuse_splits;            // single-wavefront kernels: combine splits in the kernel
     float scale_log2;           // scale * log2(e)
 };
 

@@ -1,5 +1,7 @@
 // attn_decode.hip -- paged decode attention for one query token per sequence
-// (the bulk pool's high-concurrency decode step), VALU path.
+// on the vector ALUs (TS_VARIANT_VALU).  The default for one-token decode is
+// the matrix-core kernel of attn_verify.hip, which measured faster on every
+// shape tried; this kernel stays as an explicit variant and a cross-check.
 //
 // One wavefront streams one KV head of one sequence at a time (a segment of
 // the work partition in attn_common.h) and serves all G query heads that
@@ -276,7 +278,7 @@ struct DecodeQ1 {
                     const float lse = l > 0.0f ? M + __log2f(l) : -INFINITY;
                     if (p.fuse_splits) {
                         // device-coherent stores: another worker of this
-                        // launch may combine them (see arrive)
+                        // launch may combine them (arrive_and_combine)
 #pragma unroll
                         for (int c = 0; c < NC; c++) {
                             const f32x4_t lo = {o[r][8 * c + 0] * inv, o[r][8 * c + 1] * inv,
