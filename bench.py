@@ -57,11 +57,23 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def _code_only(text: str) -> str:
+    """Source text without comments and blank-space differences, so that an
+    edit of comments alone does not count as a kernel change."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    text = re.sub(r"#[^\n]*$", lambda m: m.group(0), text, flags=re.M)
+    return " ".join(text.split())
+
+
 def kernel_hash(name: str) -> str:
     h = hashlib.sha256()
     for f in TRAFFIC_SOURCES.get(name, []):
-        with open(os.path.join(ROOT, "paper_2608_22788_amd", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2608_22788_amd", f), encoding="utf-8") as fh:
+            text = fh.read()
+        if not f.endswith(".py"):
+            text = _code_only(text)
+        h.update(text.encode())
     return h.hexdigest()[:16]
 
 
