@@ -486,6 +486,10 @@ def main():
                      "kernel_ms_mean": round(bulk["kernel_ms_mean"], 5),
                      "alg_bytes_per_launch": bulk["alg_bytes"]},
         "cpu_baseline": cpu,
+        "paper_context": {"routing_only_speedup_max": 1.67, "routing_plus_speculation_speedup_max": 2.59,
+                          "hardware": "one node of 8x NVIDIA H100, vLLM (paper Sec. 4.2, App. A.1)",
+                          "note": "end-to-end rollout speedups over uniform group routing; context only, "
+                                  "not this path's metric and not a target"},
         "tail": tail,
         "sweep": sweep,
         "makespan_model": model,

@@ -134,6 +134,22 @@ def test_workspace_reused_across_calls_and_shapes(dev, orc):
         assert int(ws[:1 << 20].count_nonzero()) == 0, f"counters left set after case {n}"
 
 
+def test_no_work_at_all():
+    """Every sequence skipped (q_lens all 0): no pages carry work, every
+    variant returns without touching the output."""
+    from paper_2608_22788_amd import device
+    import torch
+    wl = synth.make_workload("empty", seed=11, cfg=small_cfg(32, 8, 128), ctx_lens=[40, 900, 17],
+                             q_lens=[0, 0, 0], Qmax=4)
+    t = device.upload(wl)
+    for var in (0, 1, 2):
+        for w in (0, 1, 50):
+            t["out_full"].fill_(device.CANARY)
+            device.run(wl, t, num_workers=w, variant=var)
+            torch.cuda.synchronize()
+            canary_ok(t, wl)
+
+
 def test_one_key_returns_value_row_bitwise(dev, orc):
     _, device = dev
     for Qmax, var in ((1, 0), (1, 3), (2, 1), (2, 2)):
