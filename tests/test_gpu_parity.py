@@ -134,6 +134,29 @@ def test_workspace_reused_across_calls_and_shapes(dev, orc):
         assert int(ws[:1 << 20].count_nonzero()) == 0, f"counters left set after case {n}"
 
 
+@pytest.mark.parametrize("Qmax", [1, 4])
+def test_in_kernel_combine_with_many_pieces(dev, orc, Qmax):
+    """Skewed lengths so that units are plentiful (in-kernel combining is on:
+    units >= 2 x workers) while one long sequence's units are each split over
+    ~40 workers, more pieces than one combine batch holds."""
+    _, device = dev
+    ctx = [50000] + [16 + (7 * b) % 40 for b in range(99)]
+    q = [Qmax] * 100
+    wl = synth.make_workload("manypieces", seed=21, cfg=small_cfg(32, 8, 128), ctx_lens=ctx, q_lens=q,
+                             poison=True, spare_pages=1)
+    seqs = [0, 1, 50, 99]
+    ref = oracle_out(orc, wl.subset(seqs))
+    t = device.upload(wl)
+    for var in (0, 1, 3) if Qmax == 1 else (0, 1):
+        for w in (300, 397):
+            say(f"many pieces Qmax={Qmax} variant={var} workers={w}")
+            t["out_full"].fill_(device.CANARY)
+            device.run(wl, t, num_workers=w, variant=var)
+            got = device.out_as_f64(t)
+            canary_ok(t, wl)
+            assert_parity(got[seqs], ref, f"manypieces v{var} w{w}")
+
+
 def test_no_work_at_all():
     """Every sequence skipped (q_lens all 0): no pages carry work, every
     variant returns without touching the output."""
