@@ -182,7 +182,9 @@ def cpu_baseline(wl, min_seconds=10.0, max_runs=50):
     dt = (time.perf_counter() - t0) / runs
     return dict(value=wl.kv_bytes() / dt / 1e9, unit="GB/s", cores=threads, kind="oracle",
                 sample=f"whole bulk call ({wl.B} seqs, {int(wl.ctx_lens.sum())} context tokens), "
-                       f"float64, {runs} runs, {dt:.3f} s each")
+                       f"float64, {runs} runs, {dt:.3f} s each",
+                seconds_per_call=round(dt, 4), os_cpu_count=os.cpu_count(),
+                omp_num_threads=os.environ.get("OMP_NUM_THREADS"))
 
 
 def makespan_model(sweep, wl):
@@ -461,6 +463,8 @@ def main():
     cpu = None if args.no_cpu_baseline else cpu_baseline(bulk["wl"])
 
     achieved = bulk["kernel_gbps"]
+    if cpu:
+        cpu["gpu_speedup"] = round(bulk["kv_gbps"] / cpu["value"], 1)
     traffic = measured_traffic("bulk")
     line = {
         "metric": "decode-attn KV GB/s (% of HBM peak) and tokens/s vs concurrency, bulk+tail",
