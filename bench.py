@@ -25,6 +25,7 @@ import os
 import re
 import sys
 import time
+import traceback
 
 import numpy as np
 
@@ -432,38 +433,55 @@ def main():
         return
 
     bulk = time_workload("bulk", args.steps, args.warmup)
+
+    def guarded(what, fn):
+        # A failing side measurement is reported in its field; the headline
+        # line is still printed.
+        try:
+            return fn()
+        except Exception as e:   # noqa: BLE001
+            log(f"[bench] {what} failed: {e!r}")
+            traceback.print_exc(file=sys.stderr)
+            return {"error": repr(e)}
+
+    def tail_one(name):
+        r = time_workload(name, args.steps, args.warmup, MIN_WARMUP_MS)
+        r.pop("wl")
+        out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
+        out["hbm_frac"] = round(r["kv_gbps"] / PEAK_GBPS, 4)
+        out["kernel"] = KERNELS[name]
+        out["kernel_frac"] = round(r["kernel_gbps"] / PEAK_GBPS, 4)
+        out["traffic"] = measured_traffic(name)
+        return out
+
     tail = {}
     if not args.no_tail:
         for name in ("mtp", "dflash"):
-            r = time_workload(name, args.steps, args.warmup, MIN_WARMUP_MS)
-            r.pop("wl")
-            tail[name] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
-            tail[name]["hbm_frac"] = round(r["kv_gbps"] / PEAK_GBPS, 4)
-            tail[name]["kernel"] = KERNELS[name]
-            tail[name]["kernel_frac"] = round(r["kernel_gbps"] / PEAK_GBPS, 4)
-            tail[name]["traffic"] = measured_traffic(name)
+            tail[name] = guarded(name, lambda: tail_one(name))
     sweep = []
     model = None
     if not args.no_sweep:
         log(f"[bench] concurrency sweep ({args.sweep_seeds} seeds)")
-        sweep = sweep_summary(binding.concurrency_sweep(seeds=args.sweep_seeds, warmup=20, iters=30))
-        model = makespan_model(sweep, bulk["wl"])
+        sweep = guarded("sweep", lambda: sweep_summary(
+            binding.concurrency_sweep(seeds=args.sweep_seeds, warmup=20, iters=30)))
+        if isinstance(sweep, list):
+            model = guarded("makespan model", lambda: makespan_model(sweep, bulk["wl"]))
     mixed = None
     if not args.no_mixed:
         log("[bench] ragged mixed batch and graph replay")
-        mixed = mixed_and_graph()
+        mixed = guarded("mixed batch", mixed_and_graph)
     spec = None
     if not args.no_spec_step:
         log("[bench] speculative verify step: KV append, attention, acceptance")
-        spec = spec_step()
+        spec = guarded("spec step", spec_step)
     depth = None
     if not args.no_depth_sweep:
         log("[bench] draft-depth sweep (q_len 1..6 at every batch size, seed 0)")
-        depth = depth_sweep()
-    cpu = None if args.no_cpu_baseline else cpu_baseline(bulk["wl"])
+        depth = guarded("depth sweep", depth_sweep)
+    cpu = None if args.no_cpu_baseline else guarded("cpu baseline", lambda: cpu_baseline(bulk["wl"]))
 
     achieved = bulk["kernel_gbps"]
-    if cpu:
+    if cpu and "value" in cpu:
         cpu["gpu_speedup"] = round(bulk["kv_gbps"] / cpu["value"], 1)
     traffic = measured_traffic("bulk")
     line = {
