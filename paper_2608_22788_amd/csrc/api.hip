@@ -9,7 +9,9 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <map>
 #include <mutex>
+#include <tuple>
 #include <string>
 
 #include "attn_common.h"
@@ -107,29 +109,31 @@ static int auto_workers(const ts_attn_shape *s, bool q1, bool team, int rows) {
 }
 
 // Workgroups of `k` resident per compute unit times the compute units, or 0
-// if the runtime cannot tell.  Cached per kernel and device.
+// if the runtime cannot tell.  The LDS size is rounded up to 4 KiB (the
+// answer is then a lower bound, never an overestimate), so the cache keeps
+// one entry per kernel, device, block size and LDS bucket however many batch
+// sizes a caller uses.
 static int resident_workers(kernel_fn k, int threads, size_t lds) {
     static std::mutex mu;
-    struct Entry { kernel_fn k; int dev; int threads; size_t lds; int n; };
-    static Entry cache[64];
-    static int ncache = 0;
+    static std::map<std::tuple<kernel_fn, int, int, size_t>, int> cache;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess)
         return 0;
+    const size_t bucket = (lds + 4095) & ~(size_t)4095;
+    const auto key = std::make_tuple(k, dev, threads, bucket);
     std::lock_guard<std::mutex> lock(mu);
-    for (int i = 0; i < ncache; i++)
-        if (cache[i].k == k && cache[i].dev == dev && cache[i].threads == threads && cache[i].lds == lds)
-            return cache[i].n;
+    const auto it = cache.find(key);
+    if (it != cache.end())
+        return it->second;
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k), threads, lds) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(k), threads, bucket) !=
             hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
         (void)hipGetLastError();
         return 0;
     }
     const int n = per_cu * cus;
-    if (ncache < 64)
-        cache[ncache++] = Entry{k, dev, threads, lds, n};
+    cache.emplace(key, n);
     return n;
 }
 
