@@ -109,6 +109,7 @@ def make_pools(wl, n_pools):
         pools.append((k, v))
     t = device.upload(wl, values="device")
     t["k_pages"], t["v_pages"] = pools[0]
+    t["arena"] = arena
     return t, pools
 
 
@@ -119,7 +120,27 @@ def make_pools(wl, n_pools):
 MIN_WARMUP_MS = 60.0
 
 
-def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30):
+def stream_read_gbps(buf, calls=10):
+    """Sequential read ceiling: the library's streaming read over `buf`
+    (median of `calls` timed reads after 3 untimed ones)."""
+    import torch
+    from paper_2608_22788_amd import binding
+    flat = buf.view(-1).view(torch.uint8)
+    sink = torch.empty(2 << 20, dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        binding.stream_read(flat, sink)
+    ev = [(binding.Event(), binding.Event()) for _ in range(calls)]
+    for a, b in ev:
+        a.record()
+        binding.stream_read(flat, sink)
+        b.record()
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_ms(b) for a, b in ev]))
+    return dict(bytes=flat.numel(), ms=round(ms, 4), gbps=round(flat.numel() / (ms * 1e-3) / 1e9, 1))
+
+
+def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30, ceiling=True,
+                  stream_ceiling=False):
     import torch
     from paper_2608_22788_amd import binding, synth
     wl = synth.make_workload(name, seed=0)
@@ -154,15 +175,42 @@ def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30):
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / steps
     kern_ms = np.array([a.elapsed_ms(b) for a, b in ev])
+    alg = wl.algorithmic_bytes()
+    extra = {}
+    if ceiling:
+        # the same pages, the same partition and loads, no arithmetic: the
+        # ceiling of this access pattern, timed on the same rotation of pools
+        # (a failure here is reported, the attention timing is kept)
+        try:
+            sink = torch.empty(1024 * 64, dtype=torch.int32, device="cuda")
+
+            def gather(i, events=None):
+                k, v = pools[i % n_pools]
+                binding.page_gather_read(k, v, t["page_table"], t["ctx_lens"], t["q_lens"], sink,
+                                         max_ctx_len=wl.max_ctx_len, events=events)
+
+            for i in range(10):
+                gather(i)
+            for i in range(steps):
+                gather(10 + i, ev[i])
+            torch.cuda.synchronize()
+            g_ms = float(np.mean([a.elapsed_ms(b) for a, b in ev]))
+            extra = dict(gather_ms_mean=g_ms, gather_gbps=alg / (g_ms * 1e-3) / 1e9,
+                         kernel_frac_of_gather=g_ms / float(kern_ms.mean()))
+            if stream_ceiling:
+                extra["stream_read"] = stream_read_gbps(t["arena"])
+        except Exception as e:   # noqa: BLE001
+            log(f"[bench] {name}: ceiling measurement failed: {e!r}")
+            extra = dict(ceiling_error=repr(e))
     # the memory stays in torch's cache for the next workload: memory obtained
     # from the driver again after a free streams up to 5 % slower here
     del pools, t, ws
     qtok = int(wl.q_lens.sum())
-    return dict(workload=name, warmup_calls=warmup, kv_bytes=kv, alg_bytes=wl.algorithmic_bytes(), ms_per_step=ms_step,
+    return dict(workload=name, warmup_calls=warmup, kv_bytes=kv, alg_bytes=alg, ms_per_step=ms_step,
                 kernel_ms_mean=float(kern_ms.mean()), kernel_ms_median=float(np.median(kern_ms)),
                 kv_gbps=kv / (ms_step * 1e-3) / 1e9,
-                kernel_gbps=wl.algorithmic_bytes() / (kern_ms.mean() * 1e-3) / 1e9,
-                tokens_per_s=qtok / (ms_step * 1e-3), n_pools=n_pools, wl=wl)
+                kernel_gbps=alg / (kern_ms.mean() * 1e-3) / 1e9,
+                tokens_per_s=qtok / (ms_step * 1e-3), n_pools=n_pools, wl=wl, **extra)
 
 
 def cpu_baseline(wl, min_seconds=10.0, max_runs=50):
@@ -392,6 +440,24 @@ def sweep_summary(points):
     return out
 
 
+def ceiling_summary(r):
+    """Measured read ceilings beside the bulk kernel: a sequential stream read
+    and the page gather (the kernel's own pages and partition, no arithmetic)."""
+    if "ceiling_error" in r:
+        return {"error": r["ceiling_error"]}
+    if "gather_gbps" not in r:
+        return None
+    out = {"page_gather_gbps": round(r["gather_gbps"], 1),
+           "page_gather_frac_of_peak": round(r["gather_gbps"] / PEAK_GBPS, 4),
+           "kernel_frac_of_page_gather": round(r["kernel_frac_of_gather"], 4),
+           "note": "GB/s on the kernel's algorithmic bytes; the gather reads the same whole pages "
+                   "with the same partition and loads and computes nothing"}
+    if "stream_read" in r:
+        out["stream_read_gbps"] = r["stream_read"]["gbps"]
+        out["stream_read_bytes"] = r["stream_read"]["bytes"]
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -404,6 +470,8 @@ def main():
     ap.add_argument("--no-depth-sweep", action="store_true")
     ap.add_argument("--no-mixed", action="store_true")
     ap.add_argument("--no-spec-step", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the read-only ceiling kernels timed beside each workload")
     ap.add_argument("--only", choices=list(WORKLOADS), help="time one workload only (profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="with --only: first copy BYTES with the library's plain copy kernel, "
@@ -427,12 +495,12 @@ def main():
             binding.copy_bytes(dst, src)
             torch.cuda.synchronize()
             del src, dst
-        r = time_workload(args.only, args.steps, args.warmup, MIN_WARMUP_MS)
+        r = time_workload(args.only, args.steps, args.warmup, MIN_WARMUP_MS, ceiling=not args.no_ceiling)
         r.pop("wl")
         print(json.dumps(r), flush=True)
         return
 
-    bulk = time_workload("bulk", args.steps, args.warmup)
+    bulk = time_workload("bulk", args.steps, args.warmup, ceiling=not args.no_ceiling, stream_ceiling=True)
 
     def guarded(what, fn):
         # A failing side measurement is reported in its field; the headline
@@ -445,7 +513,7 @@ def main():
             return {"error": repr(e)}
 
     def tail_one(name):
-        r = time_workload(name, args.steps, args.warmup, MIN_WARMUP_MS)
+        r = time_workload(name, args.steps, args.warmup, MIN_WARMUP_MS, ceiling=not args.no_ceiling)
         r.pop("wl")
         out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
         out["hbm_frac"] = round(r["kv_gbps"] / PEAK_GBPS, 4)
@@ -508,6 +576,7 @@ def main():
                      "kernel_ms_mean": round(bulk["kernel_ms_mean"], 5),
                      "alg_bytes_per_launch": bulk["alg_bytes"]},
         "cpu_baseline": cpu,
+        "ceiling": ceiling_summary(bulk),
         "paper_context": {"routing_only_speedup_max": 1.67, "routing_plus_speculation_speedup_max": 2.59,
                           "hardware": "one node of 8x NVIDIA H100, vLLM (paper Sec. 4.2, App. A.1)",
                           "note": "end-to-end rollout speedups over uniform group routing; context only, "

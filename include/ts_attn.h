@@ -291,10 +291,32 @@ int ts_synth_page_table(int32_t batch, const int32_t *ctx_lens, int32_t page_siz
 int ts_copy_bytes(void *dst, const void *src, size_t bytes, void *stream);
 
 /* Plain streaming read of `bytes` (multiple of 16, 16-byte aligned): every
- * word is loaded once by a grid of 2,048 blocks of 256 threads, and one fold
- * per thread is written to `sink` (at least 2 MiB).  Its bandwidth is the
- * practical HBM read ceiling the attention kernels are compared with. */
+ * word is loaded once by a grid of 2,048 blocks of 256 threads, each block
+ * reading one contiguous stretch, and the XOR of the 32-bit words each thread
+ * read is written to `sink` (at least 2 MiB, uint32 per thread; the XOR of
+ * the whole sink is the XOR of every word of `src`).  Its bandwidth is the
+ * practical sequential HBM read ceiling. */
 int ts_stream_read(const void *src, size_t bytes, void *sink, size_t sink_bytes, void *stream);
+
+/* Read-only twin of ts_decode_attn: streams exactly the K and V pages a call
+ * with the same shape, pools, page table and lengths would read (the whole
+ * 16 x head_dim block of every KV head for pages 0 .. ceil(L/16) - 1 of each
+ * sequence with q_lens > 0), in the same worker partition and with the same
+ * loads, and computes nothing.  Its bandwidth is the ceiling of the paged
+ * (random 4 KiB block) access pattern on this GPU, which the attention kernels
+ * are compared with.
+ *   shape      as for ts_decode_attn (all its checks apply; num_workers 0
+ *              means 1,024 wavefronts, 4 per compute unit);
+ *   sink       device, at least workers x 64 x 4 bytes: the XOR of the 32-bit
+ *              words each lane read (the XOR of the whole sink is the XOR of
+ *              every word of the pages read);
+ *   ev_begin, ev_end  optional HIP events (NULL allowed) that take the
+ *              kernel's own start and end timestamps.
+ * Asynchronous on `stream`; device-value preconditions as for
+ * ts_decode_attn. */
+int ts_page_gather_read(const ts_attn_shape *shape, const void *k_pages, const void *v_pages,
+                        const int32_t *page_table, const int32_t *ctx_lens, const int32_t *q_lens,
+                        void *sink, size_t sink_bytes, void *stream, void *ev_begin, void *ev_end);
 
 int ts_event_create(void **ev);
 int ts_event_destroy(void *ev);

@@ -54,7 +54,7 @@ class SweepPoint(ctypes.Structure):
 
 EXPORTS = ["ts_decode_attn_workspace_size", "ts_decode_attn", "ts_decode_attn_events",
            "ts_concurrency_sweep", "ts_synth_fill_bf16", "ts_synth_sweep_lengths",
-           "ts_synth_page_table", "ts_copy_bytes", "ts_stream_read", "ts_event_create", "ts_event_destroy",
+           "ts_synth_page_table", "ts_copy_bytes", "ts_stream_read", "ts_page_gather_read", "ts_event_create", "ts_event_destroy",
            "ts_event_record", "ts_event_elapsed_ms", "ts_status_string", "ts_last_error",
            "ts_version", "ts_tau_table", "ts_replica_time", "ts_request_shares", "ts_step_makespan",
            "ts_kv_append", "ts_spec_accept_workspace_size", "ts_spec_accept"]
@@ -93,6 +93,8 @@ def _load() -> ctypes.CDLL:
     lib.ts_copy_bytes.restype = ctypes.c_int
     lib.ts_stream_read.argtypes = [P, SZ, P, SZ, P]
     lib.ts_stream_read.restype = ctypes.c_int
+    lib.ts_page_gather_read.argtypes = [pshape, P, P, P, P, P, P, SZ, P, P, P]
+    lib.ts_page_gather_read.restype = ctypes.c_int
     lib.ts_event_create.argtypes = [ctypes.POINTER(P)]
     lib.ts_event_create.restype = ctypes.c_int
     lib.ts_event_destroy.argtypes = [P]
@@ -246,6 +248,31 @@ def stream_read(src, sink, stream=None) -> None:
     n = src.numel() * src.element_size()
     check(lib.ts_stream_read(src.data_ptr(), n, sink.data_ptr(), sink.numel() * sink.element_size(),
                              _stream_ptr(stream)), "ts_stream_read")
+
+
+def page_gather_read(k_pages, v_pages, page_table, ctx_lens, q_lens, sink, max_ctx_len=None,
+                     num_workers=0, stream=None, events=None) -> None:
+    """Stream the K/V pages an attention call over the same arguments reads,
+    computing nothing (the paged-access bandwidth ceiling).  `sink` is a
+    uint32/int32 CUDA tensor of at least workers x 64 words (1,024 workers by
+    default); ``events`` = (begin, end) handles from ``Event`` time the kernel."""
+    import torch
+    for name, t, dt in (("k_pages", k_pages, torch.bfloat16), ("v_pages", v_pages, torch.bfloat16),
+                        ("page_table", page_table, torch.int32), ("ctx_lens", ctx_lens, torch.int32),
+                        ("q_lens", q_lens, torch.int32)):
+        if t.dtype != dt or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {dt} CUDA tensor")
+    if v_pages.shape != k_pages.shape:
+        raise ValueError("v_pages must match k_pages")
+    NP, Hkv, P, D = k_pages.shape
+    maxp = page_table.shape[1]
+    shape = make_shape(ctx_lens.numel(), Hkv, Hkv, D, 1, maxp, maxp * P if max_ctx_len is None else int(max_ctx_len),
+                       NP, num_workers, P)
+    ev = (None, None) if events is None else (events[0].h, events[1].h)
+    check(lib.ts_page_gather_read(ctypes.byref(shape), k_pages.data_ptr(), v_pages.data_ptr(),
+                                  page_table.data_ptr(), ctx_lens.data_ptr(), q_lens.data_ptr(),
+                                  sink.data_ptr(), sink.numel() * sink.element_size(), _stream_ptr(stream),
+                                  ev[0], ev[1]), "ts_page_gather_read")
 
 
 class Event:

@@ -137,7 +137,7 @@ static int resident_workers(kernel_fn k, int threads, size_t lds) {
     return n;
 }
 
-int make_plan(const ts_attn_shape *s, Plan *pl) {
+int check_shape(const ts_attn_shape *s) {
     if (!s)
         return fail(TS_ERR_NULL, "shape is NULL");
     if (s->num_seqs < 1 || s->num_seqs > kMaxSeqs)
@@ -172,7 +172,14 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
         return fail(TS_ERR_SHAPE, "variant %d unknown", s->variant);
     if (s->variant == TS_VARIANT_TEAM && s->head_dim != 128)
         return fail(TS_ERR_SHAPE, "the team verify kernel needs head_dim 128");
+    return TS_OK;
+}
 
+int make_plan(const ts_attn_shape *s, Plan *pl) {
+    const int st = check_shape(s);
+    if (st)
+        return st;
+    const int G = s->num_q_heads / s->num_kv_heads;
     pl->G = G;
     // The one-token VALU kernel runs only on request: the single-wavefront
     // matrix-core kernel was measured faster on one-token decode too (bulk

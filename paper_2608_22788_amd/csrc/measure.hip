@@ -1,8 +1,12 @@
 // measure.hip -- measurement helpers: a plain copy kernel (to calibrate
-// hardware byte counters against a transfer of known size) and thin wrappers
-// over HIP events so callers can time the attention kernel on its own stream.
+// hardware byte counters against a transfer of known size), two read-only
+// kernels that give the bandwidth ceilings the attention kernels are compared
+// with, and thin wrappers over HIP events so callers can time a kernel on its
+// own stream.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include "attn_common.h"
 #include "ts_attn.h"
 #include "ts_internal.h"
 
@@ -15,16 +19,81 @@ __global__ __launch_bounds__(256) void copy_kernel(uint4 *dst, const uint4 *src,
         dst[i] = src[i];
 }
 
+__device__ __forceinline__ uint32_t fold(u32x4_t v) { return v.x ^ v.y ^ v.z ^ v.w; }
+
 // Reads every 16-byte word once and folds it into one word per thread, so the
-// loads cannot be dropped; the folds are written to `sink`.
-__global__ __launch_bounds__(256) void read_kernel(const uint4 *src, int64_t n, uint32_t *sink) {
+// loads cannot be dropped; the folds are written to `sink`.  The grid sweeps
+// the buffer front to back: in step k block b reads the contiguous tile
+// k * gridDim.x + b of kReadThreads * kReadBatch words, every lane keeping
+// kReadBatch non-temporal loads in flight.
+constexpr int kReadThreads = 256;
+constexpr int kReadBatch = 8;
+
+__global__ __launch_bounds__(kReadThreads) void read_kernel(const u32x4_t *src, int64_t n, uint32_t *sink) {
+    constexpr int64_t kTile = (int64_t)kReadThreads * kReadBatch;
     uint32_t acc = 0;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const uint4 v = src[i];
-        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    for (int64_t t0 = (int64_t)blockIdx.x * kTile; t0 < n; t0 += (int64_t)gridDim.x * kTile) {
+        u32x4_t v[kReadBatch];
+#pragma unroll
+        for (int u = 0; u < kReadBatch; u++) {
+            const int64_t i = t0 + (int64_t)kReadThreads * u + threadIdx.x;
+            v[u] = ld_stream16(src + (i < n ? i : n - 1));   // clamped, not folded twice
+        }
+#pragma unroll
+        for (int u = 0; u < kReadBatch; u++)
+            if (t0 + (int64_t)kReadThreads * u + threadIdx.x < n)
+                acc ^= fold(v[u]);
     }
-    sink[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = acc;
+    sink[(size_t)blockIdx.x * kReadThreads + threadIdx.x] = acc;
+}
+
+// Reads, for every page an attention call with the same arguments streams,
+// the whole K block and V block of each KV head, in the attention kernels'
+// worker partition (attn_common.h) and with their non-temporal 16-byte loads,
+// kGatherBatch pages in flight per wavefront.  Nothing is computed beyond
+// folding the words into one per lane (written to `sink`), so its bandwidth
+// is the ceiling of the paged access pattern itself: random 32 D-byte blocks
+// found through the page table.
+constexpr int kGatherBatch = 4;
+
+template <int D>
+__global__ __launch_bounds__(kWave) void page_gather_kernel(AttnParams p, uint32_t *sink) {
+    extern __shared__ int s_pre[];
+    page_prefix(p, s_pre);
+    constexpr int kLoads = kPage * D * 2 / (16 * kWave);   // 16-byte loads per lane per block
+    const int lane = threadIdx.x;
+    const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
+    const int w = blockIdx.x;
+    const int64_t end = worker_begin(ptot, w + 1, p.W);
+    uint32_t acc = 0;
+    for (int64_t x = worker_begin(ptot, w, p.W); x < end;) {
+        const Segment s = locate(p, s_pre, x, end);
+        const int32_t *pt = p.page_table + (size_t)s.b * p.max_pages;
+        for (int j = s.j0; j < s.j1; j += kGatherBatch) {
+            u32x4_t v[kGatherBatch][2 * kLoads];
+#pragma unroll
+            for (int u = 0; u < kGatherBatch; u++) {
+                // clamped to the segment's last page (not folded twice): a
+                // load under a branch would be waited for at the join
+                const int pid = ld_meta(pt, j + u < s.j1 ? j + u : s.j1 - 1);
+                const size_t base = ((size_t)pid * p.Hkv + s.g) * (size_t)(kPage * D) + 8 * lane;
+#pragma unroll
+                for (int i = 0; i < kLoads; i++) {
+                    v[u][i] = ld_stream16(p.k_pages + base + 8 * kWave * i);
+                    v[u][kLoads + i] = ld_stream16(p.v_pages + base + 8 * kWave * i);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kGatherBatch; u++)
+                if (j + u < s.j1) {
+#pragma unroll
+                    for (int i = 0; i < 2 * kLoads; i++)
+                        acc ^= fold(v[u][i]);
+                }
+        }
+        x = s.next;
+    }
+    sink[(size_t)w * kWave + lane] = acc;
 }
 
 }  // namespace
@@ -60,19 +129,63 @@ int ts_stream_read(const void *src, size_t bytes, void *sink, size_t sink_bytes,
     clear_error();
     if (!src || !sink)
         return fail(TS_ERR_NULL, "NULL pointer");
-    if ((bytes & 15) || ((uintptr_t)src & 15))
+    if ((bytes & 15) || ((uintptr_t)src & 15) || ((uintptr_t)sink & 3))
         return fail(TS_ERR_ARG, "stream read needs 16-byte sizes and alignment");
     const int64_t blocks = 256 * 8;
-    if (sink_bytes < (size_t)blocks * 256 * sizeof(uint32_t))
-        return fail(TS_ERR_ARG, "sink needs %lld bytes", (long long)(blocks * 256 * 4));
+    if (sink_bytes < (size_t)blocks * kReadThreads * sizeof(uint32_t))
+        return fail(TS_ERR_ARG, "sink needs %lld bytes", (long long)(blocks * kReadThreads * 4));
     int st = check_device();
     if (st)
         return st;
-    hipLaunchKernelGGL(read_kernel, dim3((unsigned)blocks), dim3(256), 0,
-                       reinterpret_cast<hipStream_t>(stream), static_cast<const uint4 *>(src),
-                       (int64_t)(bytes / 16), static_cast<uint32_t *>(sink));
+    const int64_t n = (int64_t)(bytes / 16);
+    if (n == 0)
+        return TS_OK;
+    hipLaunchKernelGGL(read_kernel, dim3((unsigned)blocks), dim3(kReadThreads), 0,
+                       reinterpret_cast<hipStream_t>(stream), static_cast<const u32x4_t *>(src), n,
+                       static_cast<uint32_t *>(sink));
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? TS_OK : hip_fail(e, "stream read launch");
+}
+
+int ts_page_gather_read(const ts_attn_shape *s, const void *k_pages, const void *v_pages,
+                        const int32_t *page_table, const int32_t *ctx_lens, const int32_t *q_lens,
+                        void *sink, size_t sink_bytes, void *stream, void *ev_begin, void *ev_end) {
+    clear_error();
+    int st = check_shape(s);
+    if (st)
+        return st;
+    if (!k_pages || !v_pages || !page_table || !ctx_lens || !q_lens || !sink)
+        return fail(TS_ERR_NULL, "NULL pointer");
+    if (((uintptr_t)k_pages & 15) || ((uintptr_t)v_pages & 15) || ((uintptr_t)sink & 3))
+        return fail(TS_ERR_ARG, "misaligned pointer (pools need 16 B)");
+    const int W = s->num_workers > 0 ? s->num_workers : 256 * 4;
+    if (sink_bytes < (size_t)W * kWave * sizeof(uint32_t))
+        return fail(TS_ERR_ARG, "sink needs %zu bytes", (size_t)W * kWave * sizeof(uint32_t));
+    st = check_device();
+    if (st)
+        return st;
+    AttnParams p = {};
+    p.k_pages = static_cast<const uint16_t *>(k_pages);
+    p.v_pages = static_cast<const uint16_t *>(v_pages);
+    p.page_table = page_table;
+    p.ctx_lens = ctx_lens;
+    p.q_lens = q_lens;
+    p.B = s->num_seqs;
+    p.Hq = s->num_q_heads;
+    p.Hkv = s->num_kv_heads;
+    p.D = s->head_dim;
+    p.Qmax = s->max_q_len;
+    p.max_pages = s->max_pages_per_seq;
+    p.W = W;
+    void (*k)(AttnParams, uint32_t *) = p.D == 64 ? page_gather_kernel<64> : page_gather_kernel<128>;
+    uint32_t *out = static_cast<uint32_t *>(sink);
+    void *args[] = {&p, &out};
+    hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void *>(k), dim3(W), dim3(kWave), args,
+                                      (size_t)(p.B + 1) * sizeof(int), reinterpret_cast<hipStream_t>(stream),
+                                      reinterpret_cast<hipEvent_t>(ev_begin), reinterpret_cast<hipEvent_t>(ev_end), 0);
+    if (e == hipSuccess)
+        e = hipGetLastError();
+    return e == hipSuccess ? TS_OK : hip_fail(e, "page gather launch");
 }
 
 int ts_event_create(void **ev) {

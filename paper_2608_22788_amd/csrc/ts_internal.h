@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "ts_attn.h"
+
 namespace tsattn {
 
 struct AttnParams;
@@ -16,5 +18,8 @@ int hip_fail(hipError_t e, const char *what);
 void clear_error();
 // TS_OK if the current device is a gfx950, else TS_ERR_UNSUPPORTED / TS_ERR_HIP.
 int check_device();
+// TS_OK if every field of the shape is inside the supported set (the checks
+// of ts_decode_attn), else TS_ERR_NULL / TS_ERR_SHAPE with a message.
+int check_shape(const ts_attn_shape *s);
 
 }  // namespace tsattn
