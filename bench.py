@@ -139,11 +139,20 @@ def stream_read_gbps(buf, calls=10):
     return dict(bytes=flat.numel(), ms=round(ms, 4), gbps=round(flat.numel() / (ms * 1e-3) / 1e9, 1))
 
 
+def tp2_share(name):
+    """The per-GPU share of a two-way tensor-parallel replica of a workload:
+    half the query and KV heads, the same sequences and lengths."""
+    from paper_2608_22788_amd import synth
+    cfg = dict(synth.CONFIGS[name])
+    cfg["Hq"], cfg["Hkv"] = cfg["Hq"] // 2, cfg["Hkv"] // 2
+    return cfg
+
+
 def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30, ceiling=True,
-                  stream_ceiling=False):
+                  stream_ceiling=False, cfg=None):
     import torch
     from paper_2608_22788_amd import binding, synth
-    wl = synth.make_workload(name, seed=0)
+    wl = synth.make_workload(name, seed=0, cfg=cfg)
     kv = wl.kv_bytes()
     n_pools = max(2, -(-min_rotation // kv))
     log(f"[bench] {name}: B={wl.B} q_len={wl.Qmax} sum_ctx={int(wl.ctx_lens.sum())} "
@@ -470,6 +479,8 @@ def main():
     ap.add_argument("--no-depth-sweep", action="store_true")
     ap.add_argument("--no-mixed", action="store_true")
     ap.add_argument("--no-spec-step", action="store_true")
+    ap.add_argument("--no-shards", action="store_true",
+                    help="skip the per-GPU shares of two-way tensor-parallel replicas")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the read-only ceiling kernels timed beside each workload")
     ap.add_argument("--only", choices=list(WORKLOADS), help="time one workload only (profiling)")
@@ -526,6 +537,23 @@ def main():
     if not args.no_tail:
         for name in ("mtp", "dflash"):
             tail[name] = guarded(name, lambda: tail_one(name))
+    shards = None
+    if not args.no_shards:
+        # one GPU's share of a TP2 replica (KV heads split 8 -> 4 per GPU;
+        # attention needs no exchange, so this is the whole per-GPU step)
+        shards = {}
+        for parent in ("bulk", "dflash"):
+            def shard_one(parent=parent):
+                r = time_workload(parent + "_tp2", args.steps, args.warmup, MIN_WARMUP_MS,
+                                  ceiling=not args.no_ceiling, cfg=tp2_share(parent))
+                r.pop("wl")
+                out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
+                out["heads"] = "16 q / 4 kv"
+                out["hbm_frac"] = round(r["kv_gbps"] / PEAK_GBPS, 4)
+                out["kernel"] = KERNELS[parent]
+                out["kernel_frac"] = round(r["kernel_gbps"] / PEAK_GBPS, 4)
+                return out
+            shards[parent + "_tp2"] = guarded(parent + " tp2 share", shard_one)
     sweep = []
     model = None
     if not args.no_sweep:
@@ -582,6 +610,7 @@ def main():
                           "note": "end-to-end rollout speedups over uniform group routing; context only, "
                                   "not this path's metric and not a target"},
         "tail": tail,
+        "tp2_shares": shards,
         "sweep": sweep,
         "makespan_model": model,
         "mixed_batch": mixed,

@@ -292,6 +292,28 @@ def test_full_size_config(dev, orc, name):
         assert_parity(got[seqs], ref, f"{name} seqs {seqs} variant {var}")
 
 
+@pytest.mark.parametrize("name", ["bulk", "dflash"])
+def test_full_size_tp2_share(dev, orc, name):
+    """One GPU's share of a two-way tensor-parallel replica: the same
+    sequences with half the heads (16 query / 4 KV), sampled against the
+    oracle.  At 1,024 units for 1,024 workers the bulk share takes the merge
+    kernel instead of combining its splits in the kernel."""
+    _, device = dev
+    cfg = dict(synth.CONFIGS[name], Hq=16, Hkv=4)
+    wl = synth.make_workload(name + "_tp2", seed=0, cfg=cfg)
+    say(f"tp2 share {name}: B={wl.B} heads 16/4 sum_ctx={int(wl.ctx_lens.sum())}")
+    t = device.upload(wl, values="device")
+    seqs = sample_seqs(wl, FULL[name])
+    ref = oracle_out(orc, wl.subset(seqs))
+    for var in variants_for(wl):
+        t["out_full"].fill_(device.CANARY)
+        device.run(wl, t, variant=var)
+        got = device.out_as_f64(t)
+        canary_ok(t, wl)
+        assert np.isfinite(got).all()
+        assert_parity(got[seqs], ref, f"{name} tp2 seqs {seqs} variant {var}")
+
+
 def test_full_size_ragged_mixed_batch(dev, orc):
     """One launch over the bulk workload in which the 8 longest sequences
     verify 4 drafted tokens and the other 248 decode one (ragged q_lens under
