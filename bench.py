@@ -445,6 +445,12 @@ def sweep_summary(points):
             row[f] = round(float(xs.mean()), nd)
             row[f + "_min"] = round(float(xs.min()), nd)
             row[f + "_max"] = round(float(xs.max()), nd)
+        if all("gather_median_us" in p for p in ps):
+            # the read-only twin over the same pools: the latency floor of the call
+            g = np.array([p["kv_bytes"] / (p["gather_median_us"] * 1e-6) / 1e9 for p in ps])
+            row["gather_gbps"] = round(float(g.mean()), 1)
+            row["call_frac_of_gather"] = round(float(np.mean([p["gather_median_us"] / p["t_median_us"]
+                                                               for p in ps])), 4)
         out.append(row)
     return out
 

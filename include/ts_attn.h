@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define TS_ATTN_ABI_VERSION 1
+#define TS_ATTN_ABI_VERSION 2
 
 typedef enum ts_status {
     TS_OK = 0,
@@ -176,6 +176,8 @@ typedef struct ts_sweep_point {
     double hbm_frac;            /* kv_gbps / 8000 (MI355X HBM3E peak) */
     double tokens_per_s;        /* batch * q_len / t_median */
     double tau_us;              /* t_median / q_len: attention time per decoded position */
+    double gather_median_us;    /* per-call time of ts_page_gather_read over the same pools
+                                   (the read-only floor of the same call) */
 } ts_sweep_point;
 
 /* Runs the sweep; writes up to `cap` points (num_batches * num_seeds needed)

@@ -49,7 +49,8 @@ class SweepPoint(ctypes.Structure):
                 ("kv_bytes", ctypes.c_int64), ("t_median_us", ctypes.c_double),
                 ("t_p10_us", ctypes.c_double), ("t_p90_us", ctypes.c_double),
                 ("kv_gbps", ctypes.c_double), ("hbm_frac", ctypes.c_double),
-                ("tokens_per_s", ctypes.c_double), ("tau_us", ctypes.c_double)]
+                ("tokens_per_s", ctypes.c_double), ("tau_us", ctypes.c_double),
+                ("gather_median_us", ctypes.c_double)]
 
 
 EXPORTS = ["ts_decode_attn_workspace_size", "ts_decode_attn", "ts_decode_attn_events",

@@ -7,7 +7,9 @@
 // generator, then time ts_decode_attn with HIP events.  Calls rotate over
 // enough distinct KV pools (at least min_rotation_bytes in total) that the
 // 256 MB last-level cache cannot serve a pool from the previous call, so small
-// batches report HBM, not cache, bandwidth.
+// batches report HBM, not cache, bandwidth.  The same pools are then read by
+// ts_page_gather_read, the call's read-only twin, timed the same way: the
+// floor that latency alone sets at small batches.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -118,9 +120,11 @@ int plan_point(const ts_sweep_config &c, int32_t batch, int32_t seed, Point *pt)
 // size (memory obtained again from the driver after a free can stream a few
 // per cent slower, which would bias later points).
 struct Arena {
-    DevBuf kv, q, out, ws, tab, len, ql;
+    DevBuf kv, q, out, ws, tab, len, ql, sink;
     size_t kv_bytes = 0;
 };
+
+constexpr int kGatherWorkers = 1024;   // ts_page_gather_read's default
 
 int run_point(const ts_sweep_config &c, const Point &P, Arena &A, hipStream_t stream,
               ts_sweep_point *pt) {
@@ -148,31 +152,47 @@ int run_point(const ts_sweep_config &c, const Point &P, Arena &A, hipStream_t st
                               static_cast<const int32_t *>(A.len.p), static_cast<const int32_t *>(A.ql.p),
                               A.out.p, scale, A.ws.p, P.ws_bytes, stream);
     };
-    for (int i = 0; i < c.warmup; i++)
-        if ((st = call(i)))
-            return st;
+    auto gather = [&](int64_t i) {
+        const size_t off = (size_t)((i % pools) * pool_bytes);
+        return ts_page_gather_read(&P.sh, kbase + off, vbase + off, static_cast<const int32_t *>(A.tab.p),
+                                   static_cast<const int32_t *>(A.len.p), static_cast<const int32_t *>(A.ql.p),
+                                   A.sink.p, (size_t)kGatherWorkers * 64 * 4, stream, nullptr, nullptr);
+    };
     Events evs;
     evs.ev.resize((size_t)c.iters + 1);
     for (auto &ev : evs.ev)
         if ((e = hipEventCreate(&ev)))
             return hip_fail(e, "hipEventCreate");
-    if ((e = hipEventRecord(evs.ev[0], stream)))
-        return hip_fail(e, "hipEventRecord");
-    for (int i = 0; i < c.iters; i++) {
-        if ((st = call(c.warmup + i)))
-            return st;
-        if ((e = hipEventRecord(evs.ev[(size_t)i + 1], stream)))
-            return hip_fail(e, "hipEventRecord");
-    }
-    if ((e = hipStreamSynchronize(stream)))
-        return hip_fail(e, "hipStreamSynchronize");
-    std::vector<double> us((size_t)c.iters);
-    for (int i = 0; i < c.iters; i++) {
-        float ms = 0.f;
-        if ((e = hipEventElapsedTime(&ms, evs.ev[(size_t)i], evs.ev[(size_t)i + 1])))
-            return hip_fail(e, "hipEventElapsedTime");
-        us[(size_t)i] = 1000.0 * ms;
-    }
+    // warmup calls, then iters calls with an event after each; per-call times
+    // are the differences of consecutive events (a 0..iters-1 median)
+    auto timed = [&](auto &&fn, std::vector<double> &us) -> int {
+        int rc;
+        hipError_t he;
+        for (int i = 0; i < c.warmup; i++)
+            if ((rc = fn(i)))
+                return rc;
+        if ((he = hipEventRecord(evs.ev[0], stream)))
+            return hip_fail(he, "hipEventRecord");
+        for (int i = 0; i < c.iters; i++) {
+            if ((rc = fn(c.warmup + i)))
+                return rc;
+            if ((he = hipEventRecord(evs.ev[(size_t)i + 1], stream)))
+                return hip_fail(he, "hipEventRecord");
+        }
+        if ((he = hipStreamSynchronize(stream)))
+            return hip_fail(he, "hipStreamSynchronize");
+        us.assign((size_t)c.iters, 0.0);
+        for (int i = 0; i < c.iters; i++) {
+            float ms = 0.f;
+            if ((he = hipEventElapsedTime(&ms, evs.ev[(size_t)i], evs.ev[(size_t)i + 1])))
+                return hip_fail(he, "hipEventElapsedTime");
+            us[(size_t)i] = 1000.0 * ms;
+        }
+        return TS_OK;
+    };
+    std::vector<double> us, gus;
+    if ((st = timed(call, us)) || (st = timed(gather, gus)))
+        return st;
     pt->batch = batch;
     pt->q_len = Q;
     pt->seed = P.seed;
@@ -186,6 +206,7 @@ int run_point(const ts_sweep_config &c, const Point &P, Arena &A, hipStream_t st
     pt->hbm_frac = pt->kv_gbps / 8000.0;
     pt->tokens_per_s = (double)batch * Q / (pt->t_median_us * 1e-6);
     pt->tau_us = pt->t_median_us / Q;
+    pt->gather_median_us = quantile(gus, 0.5);
     return TS_OK;
 }
 
@@ -237,7 +258,8 @@ extern "C" int ts_concurrency_sweep(const ts_sweep_config *cfg, ts_sweep_point *
             (st = A.out.alloc(qe * 2, "hipMalloc(out)")) || (st = A.ws.alloc(ws, "hipMalloc(workspace)")) ||
             (st = A.tab.alloc(tab * 4, "hipMalloc(page table)")) ||
             (st = A.len.alloc(bmax * 4, "hipMalloc(ctx_lens)")) ||
-            (st = A.ql.alloc(bmax * 4, "hipMalloc(q_lens)")))
+            (st = A.ql.alloc(bmax * 4, "hipMalloc(q_lens)")) ||
+            (st = A.sink.alloc((size_t)kGatherWorkers * 64 * 4, "hipMalloc(gather sink)")))
             return st;
         if ((e = hipMemsetAsync(A.ws.p, 0, ws, s.s)))   // zero before its first use
             return hip_fail(e, "hipMemsetAsync(workspace)");

@@ -369,3 +369,6 @@ def test_concurrency_sweep_entry_point(dev):
         assert p["num_pools"] * p["kv_bytes"] >= (1 << 30)
         assert 0 < p["t_p10_us"] <= p["t_median_us"] <= p["t_p90_us"]
         assert p["kv_gbps"] > 0 and p["hbm_frac"] < 1.2
+        # the read-only twin over the same pools: positive, and no slower than
+        # the whole attention call by more than timing noise
+        assert 0 < p["gather_median_us"] < 1.2 * p["t_median_us"]
