@@ -17,6 +17,11 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libtsattn.so")
 
+# TS_ATTN_ABI_VERSION of the header these structures mirror: a library built
+# from another version may lay its structures out differently, so loading
+# one is refused.
+ABI_VERSION = 2
+
 TS_OK = 0
 STATUS = {0: "TS_OK", -1: "TS_ERR_NULL", -2: "TS_ERR_SHAPE", -3: "TS_ERR_WORKSPACE",
           -4: "TS_ERR_UNSUPPORTED", -5: "TS_ERR_HIP", -6: "TS_ERR_ARG"}
@@ -124,6 +129,9 @@ def _load() -> ctypes.CDLL:
     lib.ts_last_error.restype = ctypes.c_char_p
     lib.ts_version.argtypes = []
     lib.ts_version.restype = ctypes.c_int
+    if lib.ts_version() != ABI_VERSION:
+        raise ImportError(f"{LIB_PATH} has ABI version {lib.ts_version()}, this binding expects "
+                          f"{ABI_VERSION}; rebuild the library")
     return lib
 
 

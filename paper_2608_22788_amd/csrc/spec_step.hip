@@ -30,6 +30,8 @@
 //   just short of the target selects the last token with mass.
 #include <hip/hip_runtime.h>
 
+#include <climits>
+
 #include "ts_attn.h"
 #include "ts_internal.h"
 
@@ -88,10 +90,14 @@ struct AcceptParams {
     int B, V, G, nblk;
 };
 
+__device__ __forceinline__ int clamp_gamma(const AcceptParams &a, int b) {
+    const int g = a.num_draft[b];
+    return g < 0 ? 0 : (g > a.G ? a.G : g);
+}
+
 // Drafts accepted before the first rejection (gamma if none), by one thread.
 __device__ int accept_walk(const AcceptParams &a, int b) {
-    int gamma = a.num_draft[b];
-    gamma = gamma < 0 ? 0 : (gamma > a.G ? a.G : gamma);
+    const int gamma = clamp_gamma(a, b);
     for (int i = 0; i < gamma; i++) {
         const int d = a.draft[(size_t)b * a.G + i];
         if (d < 0 || d >= a.V)
@@ -103,11 +109,6 @@ __device__ int accept_walk(const AcceptParams &a, int b) {
             return i;
     }
     return gamma;
-}
-
-__device__ __forceinline__ int clamp_gamma(const AcceptParams &a, int b) {
-    const int g = a.num_draft[b];
-    return g < 0 ? 0 : (g > a.G ? a.G : g);
 }
 
 // Weights of the sampling row at elements e .. e + 3 (zero past V): the
@@ -260,11 +261,9 @@ __global__ __launch_bounds__(kPickThreads) void accept_pick_kernel(AcceptParams 
         row_weights(a, b, k, rejected, s_use_p != 0, blk * kBlk + 4 * lane, w);
         const float lane_sum = ((w[0] + w[1]) + w[2]) + w[3];
         const float incl = wave_incl_scan(lane_sum, lane);
-        const float run_total = __shfl(incl, kWave - 1, kWave);
-        // the block's total as summed by the block kernel is used for the
-        // target, so recompute it the same way
+        // the row total is taken from the block sums, as in the block search
+        // above, so that both searches aim at the same target
         const float *bs = a.bsum + ((size_t)b * 2 + (s_use_p ? 1 : 0)) * a.nblk;
-        (void)run_total;
         float total;
         {
             const int per = (a.nblk + kWave - 1) / kWave;
@@ -347,6 +346,9 @@ int ts_kv_append(const ts_attn_shape *s, const void *k_new, const void *v_new, v
     p.D = s->head_dim;
     p.max_pages = s->max_pages_per_seq;
     const int64_t total = (int64_t)p.B * p.Qmax * p.Hkv * (p.D / 8);
+    if ((total + 255) / 256 > INT32_MAX)
+        return fail(TS_ERR_SHAPE, "KV append of %lld rows is too large for one launch",
+                    (long long)((int64_t)p.B * p.Qmax * p.Hkv));
     const unsigned blocks = (unsigned)((total + 255) / 256);
     hipLaunchKernelGGL(kv_append_kernel, dim3(blocks), dim3(256), 0, reinterpret_cast<hipStream_t>(stream), p);
     hipError_t e = hipGetLastError();
@@ -397,6 +399,8 @@ int ts_spec_accept(int32_t num_seqs, int32_t vocab, int32_t max_draft, const flo
     a.nblk = (vocab + kBlk - 1) / kBlk;
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
     const int64_t waves = (int64_t)a.B * a.nblk;
+    if ((waves + 3) / 4 > INT32_MAX)
+        return fail(TS_ERR_ARG, "num_seqs x vocab is too large for one launch");
     const unsigned blocks = (unsigned)((waves + 3) / 4);
     hipLaunchKernelGGL(accept_blocks_kernel, dim3(blocks), dim3(256), 0, hs, a);
     hipError_t e = hipGetLastError();
