@@ -13,6 +13,9 @@ namespace tsattn {
 
 namespace {
 
+// One flag word per device.  The check is synchronous, but two debug calls
+// running at once on different streams of one device share it and may
+// report each other's violations.
 __device__ int g_debug_flags;
 
 enum : int {
