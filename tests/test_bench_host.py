@@ -70,3 +70,29 @@ def test_makespan_model_block(bench):
     small = L[:12].tolist()
     np.testing.assert_allclose(binding.request_shares(tau, small), om.request_shares(tau.tolist(), small),
                                rtol=1e-12)
+
+
+def test_sweep_summary_reports_the_gather_floor(bench):
+    pts = [dict(batch=1, q_len=4, seed=s, kv_gbps=500.0, hbm_frac=0.0625, tokens_per_s=1.0, tau_us=5.0,
+                kv_bytes=10_000_000, t_median_us=20.0, gather_median_us=10.0 + s) for s in range(2)]
+    r = bench.sweep_summary(pts)[0]
+    assert r["gather_gbps"] == round((1e7 / 10e-6 + 1e7 / 11e-6) / 2 / 1e9, 1)
+    assert r["call_frac_of_gather"] == round((10.0 / 20.0 + 11.0 / 20.0) / 2, 4)
+
+
+def test_tp2_share_halves_the_heads_only(bench):
+    from paper_2608_22788_amd import synth
+    for name in ("bulk", "dflash"):
+        cfg, base = bench.tp2_share(name), synth.CONFIGS[name]
+        assert (cfg["Hq"], cfg["Hkv"]) == (base["Hq"] // 2, base["Hkv"] // 2) == (16, 4)
+        assert {k: v for k, v in cfg.items() if k not in ("Hq", "Hkv")} == \
+               {k: v for k, v in base.items() if k not in ("Hq", "Hkv")}
+
+
+def test_ceiling_summary(bench):
+    r = dict(gather_gbps=6700.0, kernel_frac_of_gather=0.96, stream_read=dict(gbps=6980.0, bytes=123))
+    out = bench.ceiling_summary(r)
+    assert out["page_gather_gbps"] == 6700.0 and out["kernel_frac_of_page_gather"] == 0.96
+    assert out["stream_read_gbps"] == 6980.0 and out["page_gather_frac_of_peak"] == round(6700 / 8000, 4)
+    assert bench.ceiling_summary(dict(ceiling_error="x")) == {"error": "x"}
+    assert bench.ceiling_summary({}) is None
