@@ -217,6 +217,7 @@ def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30, 
     qtok = int(wl.q_lens.sum())
     return dict(workload=name, warmup_calls=warmup, kv_bytes=kv, alg_bytes=alg, ms_per_step=ms_step,
                 kernel_ms_mean=float(kern_ms.mean()), kernel_ms_median=float(np.median(kern_ms)),
+                kernel_ms_p10=float(np.percentile(kern_ms, 10)), kernel_ms_p90=float(np.percentile(kern_ms, 90)),
                 kv_gbps=kv / (ms_step * 1e-3) / 1e9,
                 kernel_gbps=alg / (kern_ms.mean() * 1e-3) / 1e9,
                 tokens_per_s=qtok / (ms_step * 1e-3), n_pools=n_pools, wl=wl, **extra)
@@ -608,6 +609,9 @@ def main():
                      "frac": round(achieved / PEAK_GBPS, 4), "traffic": traffic,
                      "kernel": KERNELS["bulk"],
                      "kernel_ms_mean": round(bulk["kernel_ms_mean"], 5),
+                     "kernel_ms_median": round(bulk["kernel_ms_median"], 5),
+                     "kernel_ms_p10": round(bulk["kernel_ms_p10"], 5),
+                     "kernel_ms_p90": round(bulk["kernel_ms_p90"], 5),
                      "alg_bytes_per_launch": bulk["alg_bytes"]},
         "cpu_baseline": cpu,
         "ceiling": ceiling_summary(bulk),
