@@ -96,6 +96,43 @@ def test_small_grid(dev, orc, case):
     run_case(dev, orc, wl, workers=(0, 1, 3, 40))
 
 
+def random_shape(seed):
+    """A seeded shape: KV heads, group size, head_dim, draft depth, and
+    ragged lengths that favour page boundaries (16 k - 1, 16 k, 16 k + 1)
+    and short contexts equal to q_len."""
+    rng = np.random.default_rng(1000 + seed)
+    D = int(rng.choice([64, 128]))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    while True:
+        G = int(rng.choice([1, 2, 3, 4, 6, 8, 16]))
+        Qmax = int(rng.choice([1, 2, 3, 4, 5, 6, 8, 16]))
+        if G * Qmax <= 64:
+            break
+    B = int(rng.integers(1, 24))
+    ql = rng.integers(0, Qmax + 1, size=B)
+    ql[rng.integers(0, B)] = Qmax                      # at least one full draft block
+    ctx = []
+    for q in ql:
+        kind = rng.integers(0, 4)
+        if kind == 0:
+            L = max(int(q), 1)                         # nothing but the draft block
+        elif kind == 1:
+            L = 16 * int(rng.integers(1, 40)) + int(rng.integers(-1, 2))
+        else:
+            L = int(rng.integers(1, 2500))
+        ctx.append(max(L, int(q), 1))
+    return dict(Hq=G * Hkv, Hkv=Hkv, D=D, q_lens=[int(x) for x in ql], ctx_lens=ctx, Qmax=Qmax)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_shapes(dev, orc, seed):
+    sh = random_shape(seed)
+    wl = synth.make_workload(f"rand{seed}", seed=seed, cfg=small_cfg(sh["Hq"], sh["Hkv"], sh["D"]),
+                             ctx_lens=sh["ctx_lens"], q_lens=sh["q_lens"], Qmax=sh["Qmax"], poison=True,
+                             spare_pages=1)
+    run_case(dev, orc, wl, workers=(0, 5, 333))
+
+
 @pytest.mark.parametrize("B,Qmax", [(513, 1), (1100, 4), (4096, 1)])
 def test_many_sequences(dev, orc, B, Qmax):
     """Past the 512 sequences whose lengths the partition loads in one batch,
