@@ -486,6 +486,8 @@ def main():
     ap.add_argument("--no-depth-sweep", action="store_true")
     ap.add_argument("--no-mixed", action="store_true")
     ap.add_argument("--no-spec-step", action="store_true")
+    ap.add_argument("--no-groups", action="store_true",
+                    help="skip the bulk sequences at GQA group sizes 8 and 16")
     ap.add_argument("--no-shards", action="store_true",
                     help="skip the per-GPU shares of two-way tensor-parallel replicas")
     ap.add_argument("--no-ceiling", action="store_true",
@@ -544,6 +546,27 @@ def main():
     if not args.no_tail:
         for name in ("mtp", "dflash"):
             tail[name] = guarded(name, lambda: tail_one(name))
+    groups = None
+    if not args.no_groups:
+        # the bulk sequences at larger GQA group sizes (more query rows per KV
+        # byte: G flop per byte at q_len 1), and G = 8 verifying 4 tokens
+        groups = {}
+        for Hq, Hkv, ql in ((32, 4, 1), (64, 4, 1), (32, 4, 4)):
+            key = f"bulk_g{Hq // Hkv}_q{ql}"
+
+            def group_one(Hq=Hq, Hkv=Hkv, ql=ql, key=key):
+                from paper_2608_22788_amd import synth
+                cfg = dict(synth.CONFIGS["bulk"], Hq=Hq, Hkv=Hkv, q_len=ql)
+                r = time_workload(key, args.steps, args.warmup, MIN_WARMUP_MS, ceiling=not args.no_ceiling,
+                                  cfg=cfg)
+                r.pop("wl")
+                out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
+                out["heads"] = f"{Hq} q / {Hkv} kv"
+                out["q_len"] = ql
+                out["hbm_frac"] = round(r["kv_gbps"] / PEAK_GBPS, 4)
+                out["kernel_frac"] = round(r["kernel_gbps"] / PEAK_GBPS, 4)
+                return out
+            groups[key] = guarded(key, group_one)
     shards = None
     if not args.no_shards:
         # one GPU's share of a TP2 replica (KV heads split 8 -> 4 per GPU;
@@ -621,6 +644,7 @@ def main():
                                   "not this path's metric and not a target"},
         "tail": tail,
         "tp2_shares": shards,
+        "group_sizes": groups,
         "sweep": sweep,
         "makespan_model": model,
         "mixed_batch": mixed,

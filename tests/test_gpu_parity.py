@@ -351,6 +351,26 @@ def test_full_size_tp2_share(dev, orc, name):
         assert_parity(got[seqs], ref, f"{name} tp2 seqs {seqs} variant {var}")
 
 
+@pytest.mark.parametrize("Hq,Hkv,ql", [(32, 4, 1), (64, 4, 1), (32, 4, 4)])
+def test_full_size_group_sizes(dev, orc, Hq, Hkv, ql):
+    """The bulk sequences at GQA group sizes 8 and 16 (the benchmark's
+    group_sizes field), sampled against the oracle."""
+    _, device = dev
+    cfg = dict(synth.CONFIGS["bulk"], Hq=Hq, Hkv=Hkv, q_len=ql)
+    wl = synth.make_workload(f"bulk_g{Hq // Hkv}_q{ql}", seed=0, cfg=cfg)
+    say(f"group size {Hq // Hkv}, q_len {ql}: B={wl.B} sum_ctx={int(wl.ctx_lens.sum())}")
+    t = device.upload(wl, values="device")
+    seqs = sample_seqs(wl, 3)
+    ref = oracle_out(orc, wl.subset(seqs))
+    for var in variants_for(wl):
+        t["out_full"].fill_(device.CANARY)
+        device.run(wl, t, variant=var)
+        got = device.out_as_f64(t)
+        canary_ok(t, wl)
+        assert np.isfinite(got).all()
+        assert_parity(got[seqs], ref, f"G{Hq // Hkv} q{ql} seqs {seqs} variant {var}")
+
+
 def test_full_size_ragged_mixed_batch(dev, orc):
     """One launch over the bulk workload in which the 8 longest sequences
     verify 4 drafted tokens and the other 248 decode one (ragged q_lens under
