@@ -1,7 +1,7 @@
 """The steps on either side of the verify attention in one speculative
 decoding step: writing the new tokens' keys and values into the paged cache,
-and deciding which drafted tokens the target model accepts.  Plain numpy,
-for checking only.
+and deciding which drafted tokens the target model accepts.  Plain numpy and
+Python integers, for checking only.
 
 TEST INFRASTRUCTURE ONLY: tests, the smoke check and the benchmark may call
 this module; the product library never does, and nothing here is shared with
@@ -24,22 +24,35 @@ max(0, p_k - q_k) renormalised; if every draft is accepted the next token is
 drawn from p_gamma.  The emitted tokens are then distributed exactly as the
 target model alone would produce them.
 
-Readings where the description leaves a choice:
-  * the test u <= p/q is evaluated as u * q <= p in float32 (the precision of
-    the probabilities), so both sides take the same decision; q(d) = 0 with
-    p(d) > 0 accepts, 0 <= 0 accepts (a token neither model can produce
-    never occurs in practice);
+The rule is stated over real numbers, and it is evaluated here exactly, with
+no rounding anywhere, so that any other exact evaluation gives the same
+integers:
+  * every probability is first clamped to [0, 1] (NaN read as 0) and every
+    uniform to [0, 1 - 2^-24] (NaN read as 0): probabilities are
+    float32 values, and these are the only inputs the rule is defined on;
+  * the test u <= p/q is u * q <= p over the reals (q(d) = 0 accepts, and
+    so does 0 <= 0);
   * a draft token outside the vocabulary is rejected;
-  * the next token is drawn by inverse CDF: the smallest token v whose
-    cumulative (unnormalised) mass exceeds u_sample times the total;
-  * if the leftover mass is zero (p_k == q_k up to rounding) the next token
-    is drawn from p_k itself.
+  * the next token is the smallest v whose cumulative weight
+    C_v = w_0 + ... + w_v exceeds u_sample times the total Z (inverse CDF;
+    a boundary C_v = u Z belongs to the next token).  Because u < 1 such a v
+    exists and carries weight;
+  * if the leftover mass is zero the next token is drawn from p_k itself; a
+    sampling row with no mass at all (invalid input) gives token -1.
+A float32 value in [0, 1] is an integer multiple of 2^-149 (the smallest
+positive subnormal), below 2^150 of them, so the weights and their sums are
+held as Python integers in units of 2^-149.
 """
 from __future__ import annotations
 
-from typing import Tuple
+import bisect
+import itertools
+from fractions import Fraction
 
 import numpy as np
+
+UNIT_BITS = 149                     # 2^-149: the smallest positive float32
+U_MAX = 1.0 - 2.0 ** -24            # the largest float32 below 1
 
 
 def kv_append(k_pages, v_pages, page_table, ctx_lens, q_lens, k_new, v_new, page_size=16):
@@ -56,53 +69,83 @@ def kv_append(k_pages, v_pages, page_table, ctx_lens, q_lens, k_new, v_new, page
     return k_out, v_out
 
 
+def clamp_prob(x) -> np.ndarray:
+    """float32 probabilities as float64 in [0, 1], NaN read as 0 (exact)."""
+    x = np.asarray(x, dtype=np.float32).astype(np.float64)
+    return np.clip(np.where(np.isnan(x), 0.0, x), 0.0, 1.0)
+
+
+def clamp_uniform(u) -> float:
+    """A uniform as float in [0, 1 - 2^-24], NaN read as 0."""
+    u = float(np.float32(u))
+    if not u > 0.0:
+        return 0.0
+    return min(u, U_MAX)
+
+
+def to_units(x) -> list:
+    """Exact integers x * 2^149 of float32 values already clamped to [0, 1].
+    Scaling a float64 by a power of two is exact here (no overflow), and the
+    result is an integer-valued float, which int() converts exactly."""
+    return [int(v) for v in (np.asarray(x, dtype=np.float64) * 2.0 ** UNIT_BITS).tolist()]
+
+
 def accept_walk(p_target, q_draft, draft, gamma, u_accept) -> int:
-    """Number of leading drafts accepted for one sequence."""
+    """Number of leading drafts accepted for one sequence (exact test)."""
     V = p_target.shape[-1]
     for i in range(gamma):
         d = int(draft[i])
         if d < 0 or d >= V:
             return i
-        lhs = np.float32(u_accept[i]) * np.float32(q_draft[i, d])
-        if not lhs <= np.float32(p_target[i, d]):
+        u = Fraction(clamp_uniform(u_accept[i]))
+        q = Fraction(float(clamp_prob(q_draft[i, d])))
+        p = Fraction(float(clamp_prob(p_target[i, d])))
+        if not u * q <= p:
             return i
     return gamma
 
 
-def sample_inverse_cdf(weights: np.ndarray, u: float, tol: float = 1e-5) -> Tuple[int, bool]:
-    """Smallest v with cumsum(weights)[v] > u * sum(weights), in float64;
-    also whether u * sum lies within tol * sum of a cumulative boundary (then
-    a float32 evaluation may pick a neighbour)."""
-    w = np.asarray(weights, dtype=np.float64)
-    c = np.cumsum(w)
-    Z = c[-1]
-    target = float(u) * Z
-    v = int(np.searchsorted(c, target, side="right"))
-    v = min(v, len(w) - 1)
-    while w[v] == 0.0 and v > 0:            # never land on a zero-mass token
-        v -= 1
-    near = bool(np.any(np.abs(c - target) <= tol * Z))
-    return v, near
+def sampling_weights(p_row, q_row=None) -> list:
+    """Integer weights (units of 2^-149): max(0, p - q), or p if q_row is None."""
+    P = to_units(clamp_prob(p_row))
+    if q_row is None:
+        return P
+    Q = to_units(clamp_prob(q_row))
+    return [a - b if a > b else 0 for a, b in zip(P, Q)]
 
 
-def spec_accept(p_target, q_draft, draft_tokens, num_draft, u_accept, u_sample, tol=1e-5):
-    """Per sequence: (accepted draft count, next token, decision near a
-    boundary).  p_target [B][Gmax+1][V], q_draft [B][Gmax][V] (float32
-    probabilities), draft_tokens [B][Gmax], num_draft [B], u_accept [B][Gmax],
-    u_sample [B]."""
+def sample_inverse_cdf(weights: list, u: float) -> int:
+    """Smallest v with w_0 + ... + w_v > u * sum(w), exactly (weights are
+    integers); -1 if the weights sum to zero."""
+    C = list(itertools.accumulate(weights))
+    Z = C[-1] if C else 0
+    if Z == 0:
+        return -1
+    target = Fraction(clamp_uniform(u)) * Z
+    # C_v > target  <=>  C_v > floor(target), as C_v is an integer
+    return bisect.bisect_right(C, int(target))
+
+
+def spec_accept(p_target, q_draft, draft_tokens, num_draft, u_accept, u_sample):
+    """Per sequence: (accepted draft count, next token).  p_target
+    [B][Gmax+1][V], q_draft [B][Gmax][V] (float32 probabilities),
+    draft_tokens [B][Gmax], num_draft [B], u_accept [B][Gmax], u_sample [B].
+    num_draft is clamped to [0, Gmax]."""
+    p_target = np.asarray(p_target)
+    Gmax = p_target.shape[1] - 1
     B = len(num_draft)
     n_acc = np.zeros(B, dtype=np.int32)
     nxt = np.zeros(B, dtype=np.int32)
-    near = np.zeros(B, dtype=bool)
     for b in range(B):
-        g = int(num_draft[b])
-        k = accept_walk(p_target[b], q_draft[b], draft_tokens[b], g, u_accept[b])
+        g = min(max(int(num_draft[b]), 0), Gmax)
+        k = accept_walk(p_target[b], q_draft[b] if g else None, draft_tokens[b] if g else None, g,
+                        u_accept[b] if g else None)
         n_acc[b] = k
         if k < g:
-            w = np.maximum(0.0, p_target[b, k].astype(np.float64) - q_draft[b, k].astype(np.float64))
-            if w.sum() <= 0.0:
-                w = p_target[b, k].astype(np.float64)
+            w = sampling_weights(p_target[b, k], q_draft[b, k])
+            if sum(w) == 0:
+                w = sampling_weights(p_target[b, k])
         else:
-            w = p_target[b, g].astype(np.float64)
-        nxt[b], near[b] = sample_inverse_cdf(w, float(u_sample[b]), tol)
-    return n_acc, nxt, near
+            w = sampling_weights(p_target[b, g])
+        nxt[b] = sample_inverse_cdf(w, float(u_sample[b]))
+    return n_acc, nxt
