@@ -209,21 +209,27 @@ int ts_kv_append(const ts_attn_shape *shape, const void *k_new, const void *v_ne
 size_t ts_spec_accept_workspace_size(int32_t num_seqs, int32_t vocab);
 
 /* Lossless acceptance (speculative sampling, Leviathan et al. 2023, which
- * the paper follows).  Sequence b proposed gamma_b = num_draft[b] (<=
- * max_draft) tokens d_i = draft_tokens[b][i] drawn from the drafter's
- * distributions q_draft[b][i][:]; the verify pass gave the target's
+ * the paper follows in Sec. 3.4).  Sequence b proposed gamma_b = num_draft[b]
+ * (clamped to 0 .. max_draft) tokens d_i = draft_tokens[b][i] drawn from the
+ * drafter's distributions q_draft[b][i][:]; the verify pass gave the target's
  * distributions p_target[b][i][:] for i = 0 .. gamma_b (row gamma_b follows
- * the last draft).  Draft i is accepted while u_accept[b][i] * q <= p (fp32;
- * a draft id outside [0, vocab) is rejected); at the first rejection k the
- * next token is drawn from max(0, p_k - q_k) (from p_k if that is all zero),
- * after full acceptance from p_gamma, as the smallest token whose cumulative
- * mass exceeds u_sample[b] times the total.  Writes num_accepted[b] (0 ..
- * gamma_b) and next_token[b].
+ * the last draft).  Draft i is accepted while u_accept[b][i] * q <= p (a
+ * draft id outside [0, vocab) is rejected); at the first rejection k the next
+ * token is drawn from max(0, p_k - q_k) (from p_k if that is all zero), after
+ * full acceptance from p_gamma, as the smallest token whose cumulative mass
+ * exceeds u_sample[b] times the total.  The rule is evaluated exactly, with no
+ * rounding (the test on float64 products of the float32 inputs, the masses as
+ * integers in units of 2^-149), so the result does not depend on summation
+ * order.  Probabilities are clamped to [0, 1] and uniforms to [0, 1 - 2^-24],
+ * NaN read as 0.  Writes num_accepted[b] (0 .. gamma_b) and next_token[b]
+ * (-1 if the sampling row has no mass at all).
  *   p_target  fp32 [num_seqs][max_draft + 1][vocab], 16-byte aligned
  *   q_draft   fp32 [num_seqs][max_draft][vocab] (may be NULL if max_draft 0)
  *   draft_tokens, u_accept  [num_seqs][max_draft];  num_draft, u_sample,
  *   num_accepted, next_token  [num_seqs]; uniforms in [0, 1).
- * The caller supplies the random numbers, so results are reproducible. */
+ * The caller supplies the random numbers, so results are reproducible.  The
+ * workspace (ts_spec_accept_workspace_size bytes, 256-byte aligned, any
+ * contents) holds the exact block sums. */
 int ts_spec_accept(int32_t num_seqs, int32_t vocab, int32_t max_draft, const float *p_target,
                    const float *q_draft, const int32_t *draft_tokens, const int32_t *num_draft,
                    const float *u_accept, const float *u_sample, int32_t *num_accepted,

@@ -11,23 +11,29 @@
 //   * acceptance: per sequence, walk the drafts while u_i * q_i(d_i) <=
 //     p_i(d_i); at the first rejection k draw the next token from the
 //     leftover mass max(0, p_k - q_k), after full acceptance from the bonus
-//     row p_gamma, by inverse CDF with the caller's uniform.  The sampling row
-//     is a full vocabulary of fp32 probabilities per sequence, so the work is
-//     a streaming read of one or two rows:
+//     row p_gamma, by inverse CDF with the caller's uniform.  The rule is
+//     stated over real numbers and is evaluated here without rounding: the
+//     test u q <= p on float64 products (exact for float32 factors), and the
+//     weights and their running sums as integers in units of 2^-149, the
+//     smallest float32, held in three 64-bit words (Fx below).  So the result
+//     does not depend on the order of the sums, and the parallel evaluation
+//     gives exactly the sequential one.  The sampling row is a full
+//     vocabulary of fp32 probabilities per sequence, so the work is a
+//     streaming read of one or two rows:
 //       - accept_blocks_kernel: every 256-element block of every sequence's
-//         sampling row is summed by one wavefront (a float4 per lane, lane
-//         sums in element order, then a butterfly), so the whole chip shares
-//         the read even for a handful of sequences;
-//       - accept_pick_kernel: one workgroup per sequence scans the block sums
+//         sampling row is summed by one wavefront (a float4 per lane, then a
+//         butterfly), so the whole chip shares the read even for a handful
+//         of sequences;
+//       - accept_pick_kernel: one wavefront per sequence scans the block sums
 //         (lane runs of consecutive blocks, a wavefront scan of the run
-//         totals), finds the block where the cumulative mass passes
-//         u * total, and scans that block's 256 elements in order.
+//         totals), finds the block where the cumulative mass first exceeds
+//         floor(u * total), and scans that block's 256 elements.
 //     Both kernels recompute the acceptance walk (2 gamma scalar loads)
 //     rather than pass it through memory.
-//   Readings: the acceptance test is taken in fp32 as u * q <= p; a draft id
-//   outside [0, V) is rejected; if the leftover mass sums to zero the next
-//   token is drawn from p_k itself; a cumulative mass that rounding leaves
-//   just short of the target selects the last token with mass.
+//   Readings: probabilities are clamped to [0, 1] and uniforms to
+//   [0, 1 - 2^-24], NaN read as 0; a draft id outside [0, V) is rejected; if
+//   the leftover mass is zero the next token is drawn from p_k itself; a
+//   sampling row without mass gives token -1.
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -86,16 +92,147 @@ struct AcceptParams {
     const float *u_accept;   // [B][G]
     const float *u_sample;   // [B]
     int32_t *n_accepted, *next_token;
-    float *bsum;             // [B][nblk] block sums of the sampling row
+    uint64_t *bsum;          // [B][2][nblk][3] exact block sums of the sampling row
     int B, V, G, nblk;
 };
+
+// ---- exact fixed point --------------------------------------------------------
+// A float32 in [0, 1] is an integer number of units of 2^-149 (the smallest
+// positive subnormal), below 2^150 of them; a row of at most 2^31 such
+// weights sums to below 2^181.  Fx holds such integers in three 64-bit words,
+// so every sum and comparison below is exact and independent of order.
+struct Fx {
+    uint64_t w0, w1, w2;
+};
+
+__device__ __forceinline__ Fx fx_zero() { return Fx{0, 0, 0}; }
+
+__device__ __forceinline__ Fx fx_add(Fx a, Fx b) {
+    Fx r;
+    r.w0 = a.w0 + b.w0;
+    const uint64_t c0 = r.w0 < a.w0;
+    const uint64_t t = a.w1 + b.w1;
+    uint64_t c1 = t < a.w1;
+    r.w1 = t + c0;
+    c1 += r.w1 < t;
+    r.w2 = a.w2 + b.w2 + c1;
+    return r;
+}
+
+__device__ __forceinline__ bool fx_gt(Fx a, Fx b) {
+    if (a.w2 != b.w2)
+        return a.w2 > b.w2;
+    if (a.w1 != b.w1)
+        return a.w1 > b.w1;
+    return a.w0 > b.w0;
+}
+
+__device__ __forceinline__ bool fx_is_zero(Fx a) { return (a.w0 | a.w1 | a.w2) == 0; }
+
+// a - b for a > b.
+__device__ __forceinline__ Fx fx_sub(Fx a, Fx b) {
+    Fx r;
+    r.w0 = a.w0 - b.w0;
+    const uint64_t b0 = a.w0 < b.w0;
+    const uint64_t t = a.w1 - b.w1;
+    uint64_t b1 = a.w1 < b.w1;
+    r.w1 = t - b0;
+    b1 += t < b0;
+    r.w2 = a.w2 - b.w2 - b1;
+    return r;
+}
+
+// A probability clamped to [0, 1] (NaN and negatives read as 0), in units of
+// 2^-149: significand M (with the implicit bit for normal numbers) shifted
+// left by (biased exponent - 1), at most 126.
+__device__ __forceinline__ Fx fx_of_prob(float x) {
+    x = x > 0.0f ? fminf(x, 1.0f) : 0.0f;
+    const uint32_t bits = __float_as_uint(x);
+    const uint32_t e = bits >> 23, f = bits & 0x7fffffu;
+    const uint64_t M = e ? (uint64_t)(f | 0x800000u) : (uint64_t)f;
+    const uint32_t sh = e ? e - 1 : 0;
+    const uint32_t off = sh & 63;
+    const uint64_t lo = M << off;
+    const uint64_t hi = off ? M >> (64 - off) : 0;
+    return sh < 64 ? Fx{lo, hi, 0} : Fx{0, lo, hi};
+}
+
+// A uniform clamped to [0, 1 - 2^-24] (NaN and negatives read as 0).
+__device__ __forceinline__ float clamp_uniform(float u) {
+    return u > 0.0f ? fminf(u, 0x1.fffffep-1f) : 0.0f;
+}
+
+// floor(u * Z) for a clamped uniform u: u = m 2^-s with m < 2^24 and
+// s >= 24, so m Z < 2^205 takes four words before the shift.
+__device__ __forceinline__ Fx fx_floor_mul(Fx Z, float u) {
+    const uint32_t bits = __float_as_uint(u);
+    const uint32_t e = bits >> 23, f = bits & 0x7fffffu;
+    const uint64_t m = e ? (uint64_t)(f | 0x800000u) : (uint64_t)f;
+    const uint32_t s = e ? 150 - e : 149;
+    uint64_t r[4];
+    const uint64_t lo0 = m * Z.w0, hi0 = __umul64hi(m, Z.w0);
+    const uint64_t lo1 = m * Z.w1, hi1 = __umul64hi(m, Z.w1);
+    const uint64_t lo2 = m * Z.w2, hi2 = __umul64hi(m, Z.w2);
+    r[0] = lo0;
+    r[1] = lo1 + hi0;
+    const uint64_t c1 = r[1] < lo1;
+    const uint64_t t = lo2 + hi1;
+    uint64_t c2 = t < lo2;
+    r[2] = t + c1;
+    c2 += r[2] < t;
+    r[3] = hi2 + c2;
+    const uint32_t ws = s >> 6, bs = s & 63;
+    uint64_t out[3];
+#pragma unroll
+    for (int i = 0; i < 3; i++) {
+        // words i + ws and i + ws + 1 of r (zero past the top), selected
+        // without dynamic indexing
+        uint64_t a = 0, b = 0;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            a = (uint32_t)(i + (int)ws) == (uint32_t)j ? r[j] : a;
+            b = (uint32_t)(i + (int)ws + 1) == (uint32_t)j ? r[j] : b;
+        }
+        out[i] = (a >> bs) | (bs ? b << (64 - bs) : 0);
+    }
+    return Fx{out[0], out[1], out[2]};
+}
+
+__device__ __forceinline__ Fx fx_shfl_xor(Fx a, int m) {
+    return Fx{__shfl_xor(a.w0, m, kWave), __shfl_xor(a.w1, m, kWave), __shfl_xor(a.w2, m, kWave)};
+}
+__device__ __forceinline__ Fx fx_shfl_up(Fx a, int d) {
+    return Fx{__shfl_up(a.w0, d, kWave), __shfl_up(a.w1, d, kWave), __shfl_up(a.w2, d, kWave)};
+}
+__device__ __forceinline__ Fx fx_shfl(Fx a, int lane) {
+    return Fx{__shfl(a.w0, lane, kWave), __shfl(a.w1, lane, kWave), __shfl(a.w2, lane, kWave)};
+}
+
+__device__ __forceinline__ Fx wave_sum(Fx x) {
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1)
+        x = fx_add(x, fx_shfl_xor(x, m));
+    return x;
+}
+
+// Inclusive scan over a wavefront.
+__device__ __forceinline__ Fx wave_incl_scan(Fx x, int lane) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const Fx y = fx_shfl_up(x, d);
+        if (lane >= d)
+            x = fx_add(x, y);
+    }
+    return x;
+}
 
 __device__ __forceinline__ int clamp_gamma(const AcceptParams &a, int b) {
     const int g = a.num_draft[b];
     return g < 0 ? 0 : (g > a.G ? a.G : g);
 }
 
-// Drafts accepted before the first rejection (gamma if none), by one thread.
+// Drafts accepted before the first rejection (gamma if none).  The test
+// u q <= p is exact: the product of two float32 values is exact in float64.
 __device__ int accept_walk(const AcceptParams &a, int b) {
     const int gamma = clamp_gamma(a, b);
     for (int i = 0; i < gamma; i++) {
@@ -104,56 +241,65 @@ __device__ int accept_walk(const AcceptParams &a, int b) {
             return i;
         const float pv = a.p[((size_t)b * (a.G + 1) + i) * a.V + d];
         const float qv = a.q[((size_t)b * a.G + i) * a.V + d];
-        const float u = a.u_accept[(size_t)b * a.G + i];
-        if (!(u * qv <= pv))
+        const float p = pv > 0.0f ? fminf(pv, 1.0f) : 0.0f;
+        const float q = qv > 0.0f ? fminf(qv, 1.0f) : 0.0f;
+        const float u = clamp_uniform(a.u_accept[(size_t)b * a.G + i]);
+        if (!((double)u * (double)q <= (double)p))
             return i;
     }
     return gamma;
 }
 
-// Weights of the sampling row at elements e .. e + 3 (zero past V): the
-// leftover mass at a rejection (use_p = false), else the target row itself.
+// Exact weights of the sampling row at elements e .. e + 3 (zero past V): the
+// leftover mass max(0, p_k - q_k) at a rejection (use_p = false), else the
+// target row itself.
 __device__ __forceinline__ void row_weights(const AcceptParams &a, int b, int k, bool rejected, bool use_p,
-                                           int e, float w[4]) {
+                                           int e, Fx w[4]) {
     const float *prow = a.p + ((size_t)b * (a.G + 1) + k) * a.V;
     const float *qrow = a.q + ((size_t)b * a.G + (rejected ? k : 0)) * a.V;
+    const bool resid = rejected && !use_p;
+    float pe[4], qe[4];
     if (e + 3 < a.V && ((a.V & 3) == 0)) {
         const float4 pv = *reinterpret_cast<const float4 *>(prow + e);
-        float pe[4] = {pv.x, pv.y, pv.z, pv.w};
-        if (rejected && !use_p) {
+        pe[0] = pv.x; pe[1] = pv.y; pe[2] = pv.z; pe[3] = pv.w;
+        if (resid) {
             const float4 qv = *reinterpret_cast<const float4 *>(qrow + e);
-            const float qe[4] = {qv.x, qv.y, qv.z, qv.w};
-#pragma unroll
-            for (int j = 0; j < 4; j++)
-                pe[j] = fmaxf(0.0f, pe[j] - qe[j]);
+            qe[0] = qv.x; qe[1] = qv.y; qe[2] = qv.z; qe[3] = qv.w;
         }
+    } else {
 #pragma unroll
-        for (int j = 0; j < 4; j++)
-            w[j] = pe[j];
-        return;
+        for (int j = 0; j < 4; j++) {
+            const bool in = e + j < a.V;
+            pe[j] = in ? prow[e + j] : 0.0f;
+            qe[j] = (in && resid) ? qrow[e + j] : 0.0f;
+        }
     }
 #pragma unroll
     for (int j = 0; j < 4; j++) {
-        const int v = e + j;
-        if (v >= a.V) {
-            w[j] = 0.0f;
-            continue;
+        const Fx P = fx_of_prob(pe[j]);
+        if (resid) {
+            const Fx Q = fx_of_prob(qe[j]);
+            w[j] = fx_gt(P, Q) ? fx_sub(P, Q) : fx_zero();
+        } else {
+            w[j] = P;
         }
-        const float pv = prow[v];
-        w[j] = (rejected && !use_p) ? fmaxf(0.0f, pv - qrow[v]) : pv;
     }
 }
 
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1)
-        x += __shfl_xor(x, off, kWave);
-    return x;
+__device__ __forceinline__ Fx sum4(const Fx w[4]) {
+    return fx_add(fx_add(w[0], w[1]), fx_add(w[2], w[3]));
 }
 
-// One wavefront per (sequence, block): the block's sum of sampling weights.
-// The leftover-mass and plain-row sums are both written when a rejection
-// happened, so the pick kernel can fall back without another pass.
+__device__ __forceinline__ void store_fx(uint64_t *p, Fx x) {
+    p[0] = x.w0;
+    p[1] = x.w1;
+    p[2] = x.w2;
+}
+__device__ __forceinline__ Fx load_fx(const uint64_t *p) { return Fx{p[0], p[1], p[2]}; }
+
+// One wavefront per (sequence, block): the block's exact sum of sampling
+// weights.  The leftover-mass and plain-row sums are both written when a
+// rejection happened, so the pick kernel can fall back without another pass.
 __global__ __launch_bounds__(256) void accept_blocks_kernel(AcceptParams a) {
     const int wave = (int)(blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave);
     const int lane = threadIdx.x % kWave;
@@ -163,148 +309,101 @@ __global__ __launch_bounds__(256) void accept_blocks_kernel(AcceptParams a) {
     const int gamma = clamp_gamma(a, b);
     const int k = accept_walk(a, b);
     const bool rejected = k < gamma;
-    float w[4];
+    Fx w[4];
     row_weights(a, b, k, rejected, false, blk * kBlk + 4 * lane, w);
-    const float s = wave_sum(((w[0] + w[1]) + w[2]) + w[3]);
+    const Fx s = wave_sum(sum4(w));
     if (lane == 0)
-        a.bsum[((size_t)b * 2 + 0) * a.nblk + blk] = s;
+        store_fx(a.bsum + (((size_t)b * 2 + 0) * a.nblk + blk) * 3, s);
     if (rejected) {
         row_weights(a, b, k, true, true, blk * kBlk + 4 * lane, w);
-        const float sp = wave_sum(((w[0] + w[1]) + w[2]) + w[3]);
+        const Fx sp = wave_sum(sum4(w));
         if (lane == 0)
-            a.bsum[((size_t)b * 2 + 1) * a.nblk + blk] = sp;
+            store_fx(a.bsum + (((size_t)b * 2 + 1) * a.nblk + blk) * 3, sp);
     }
 }
 
-// Inclusive scan over a wavefront.
-__device__ __forceinline__ float wave_incl_scan(float x, int lane) {
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const float y = __shfl_up(x, off, kWave);
-        if (lane >= off)
-            x += y;
-    }
-    return x;
-}
-
+// One wavefront per sequence: the total, the target T = floor(u Z), the block
+// whose cumulative mass first exceeds T, and the element inside it.  Since the
+// cumulative weights are integers, C_v > u Z exactly when C_v > T, and u < 1
+// makes T < Z, so the element exists and carries weight.
 __global__ __launch_bounds__(kPickThreads) void accept_pick_kernel(AcceptParams a) {
-    __shared__ int s_k;
-    __shared__ int s_blk;
-    __shared__ float s_base;
-    __shared__ int s_use_p;
     const int b = blockIdx.x;
-    const int tid = threadIdx.x;
-    const int lane = tid % kWave;
-    if (tid == 0) {
-        s_k = accept_walk(a, b);
-        s_blk = -1;
-    }
-    __syncthreads();
+    const int lane = threadIdx.x;
     const int gamma = clamp_gamma(a, b);
-    const int k = s_k;
+    const int k = __builtin_amdgcn_readfirstlane(accept_walk(a, b));
     const bool rejected = k < gamma;
+    const int per = (a.nblk + kWave - 1) / kWave;   // consecutive blocks per lane
+    const int lo = min(lane * per, a.nblk), hi = min(lo + per, a.nblk);
 
-    // which block holds the target mass
-    {
-        int use_p = 0;
-        for (int pass = 0; pass < 2; pass++) {
-            const float *bs = a.bsum + ((size_t)b * 2 + pass) * a.nblk;
-            const int per = (a.nblk + kWave - 1) / kWave;   // consecutive blocks per lane
-            const int lo = lane * per, hi = min(lo + per, a.nblk);
-            float run = 0.0f;
-            for (int j = lo; j < hi; j++)
-                run += bs[j];
-            const float incl = wave_incl_scan(run, lane);
-            const float total = __shfl(incl, kWave - 1, kWave);
-            if (pass == 0 && !(total > 0.0f) && rejected) {
-                use_p = 1;   // leftover mass vanished: sample p_k itself
-                continue;
-            }
-            const float target = a.u_sample[b] * total;
-            // the lane whose run holds the target, else the last lane with mass
-            const float excl = incl - run;
-            const bool here = run > 0.0f && excl <= target && target < incl;
-            const unsigned long long m = __ballot(here);
-            const unsigned long long nz = __ballot(run > 0.0f);
-            const int owner = m ? __ffsll((long long)m) - 1 : (nz ? 63 - __clzll((long long)nz) : 0);
-            if (lane == owner) {
-                float acc = excl;
-                int pick = -1, last = -1;
-                for (int j = lo; j < hi; j++) {
-                    if (bs[j] > 0.0f) {
-                        last = j;
-                        if (pick < 0 && target < acc + bs[j])
-                            pick = j;
-                    }
-                    if (pick < 0)
-                        acc += bs[j];
-                }
-                if (pick < 0) {
-                    pick = last < 0 ? 0 : last;
-                    acc = excl;
-                    for (int j = lo; j < pick; j++)
-                        acc += bs[j];
-                }
-                s_blk = pick;
-                s_base = acc;
-                s_use_p = use_p;
-            }
-            break;
-        }
+    int pass = 0;
+    Fx run, incl, Z;
+    const uint64_t *bs = nullptr;
+    for (;; pass++) {
+        bs = a.bsum + ((size_t)b * 2 + pass) * a.nblk * 3;
+        run = fx_zero();
+        for (int j = lo; j < hi; j++)
+            run = fx_add(run, load_fx(bs + 3 * (size_t)j));
+        incl = wave_incl_scan(run, lane);
+        Z = fx_shfl(incl, kWave - 1);
+        // leftover mass zero: sample p_k itself (its sums are in pass 1)
+        if (pass == 0 && rejected && fx_is_zero(Z))
+            continue;
+        break;
     }
-    __syncthreads();
-
-    // the element inside that block, scanned in order
-    {
-        const int blk = s_blk;
-        float w[4];
-        row_weights(a, b, k, rejected, s_use_p != 0, blk * kBlk + 4 * lane, w);
-        const float lane_sum = ((w[0] + w[1]) + w[2]) + w[3];
-        const float incl = wave_incl_scan(lane_sum, lane);
-        // the row total is taken from the block sums, as in the block search
-        // above, so that both searches aim at the same target
-        const float *bs = a.bsum + ((size_t)b * 2 + (s_use_p ? 1 : 0)) * a.nblk;
-        float total;
-        {
-            const int per = (a.nblk + kWave - 1) / kWave;
-            const int lo = lane * per, hi = min(lo + per, a.nblk);
-            float run = 0.0f;
-            for (int j = lo; j < hi; j++)
-                run += bs[j];
-            total = __shfl(wave_incl_scan(run, lane), kWave - 1, kWave);
-        }
-        const float target = a.u_sample[b] * total;
-        float acc = s_base + (incl - lane_sum);
-        int pick = -1;
-        int j = 0;
-        for (; j < 4; j++) {
-            if (w[j] > 0.0f && target < acc + w[j]) {
-                pick = j;
-                break;
-            }
-            acc += w[j];
-        }
-        const bool found = pick >= 0;
-        const unsigned long long m = __ballot(found);
-        int last_lane = -1, last_j = -1;
-        if (!m) {
-            // rounding left the walk short: the block's last element with mass
-            int lj = -1;
-            for (int jj = 3; jj >= 0; jj--)
-                if (w[jj] > 0.0f) {
-                    lj = jj;
-                    break;
-                }
-            const unsigned long long nz = __ballot(lj >= 0);
-            last_lane = nz ? 63 - __clzll((long long)nz) : 0;
-            last_j = __shfl(lj, last_lane, kWave);
-        }
-        const int first = m ? __ffsll((long long)m) - 1 : last_lane;
-        const int jsel = m ? __shfl(pick, first, kWave) : (last_j < 0 ? 0 : last_j);
+    if (fx_is_zero(Z)) {
         if (lane == 0) {
             a.n_accepted[b] = k;
-            a.next_token[b] = blk * kBlk + 4 * first + jsel;
+            a.next_token[b] = -1;   // a sampling row with no mass
         }
+        return;
+    }
+    const Fx T = fx_floor_mul(Z, clamp_uniform(a.u_sample[b]));
+
+    // the first lane whose run ends above T owns the block
+    const unsigned long long own = __ballot(fx_gt(incl, T));
+    const int owner = __ffsll((long long)own) - 1;   // exists: incl of lane 63 = Z > T
+    int blk = 0;
+    Fx base = fx_zero();
+    if (lane == owner) {
+        Fx acc = fx_sub(incl, run);   // mass before this lane's run (incl >= run)
+        for (int j = lo; j < hi; j++) {
+            const Fx next = fx_add(acc, load_fx(bs + 3 * (size_t)j));
+            if (fx_gt(next, T)) {
+                blk = j;
+                break;
+            }
+            acc = next;
+        }
+        base = acc;
+    }
+    blk = __shfl(blk, owner, kWave);
+    base = fx_shfl(base, owner);
+
+    // the element inside that block
+    Fx w[4];
+    row_weights(a, b, k, rejected, pass == 1, blk * kBlk + 4 * lane, w);
+    const Fx lane_sum = sum4(w);
+    const Fx lincl = fx_add(base, wave_incl_scan(lane_sum, lane));
+    const unsigned long long hit = __ballot(fx_gt(lincl, T));
+    const int first = __ffsll((long long)hit) - 1;   // exists: the block's total exceeds T
+    int jsel = 3;
+    if (lane == first) {
+        // the smallest j whose cumulative weight exceeds T
+        Fx acc = fx_sub(lincl, lane_sum);
+        bool found = false;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            acc = fx_add(acc, w[j]);
+            if (!found && fx_gt(acc, T)) {
+                jsel = j;
+                found = true;
+            }
+        }
+    }
+    jsel = __shfl(jsel, first, kWave);
+    if (lane == 0) {
+        a.n_accepted[b] = k;
+        a.next_token[b] = blk * kBlk + 4 * first + jsel;
     }
 }
 
@@ -362,7 +461,7 @@ size_t ts_spec_accept_workspace_size(int32_t num_seqs, int32_t vocab) {
         return 0;
     }
     const size_t nblk = ((size_t)vocab + kBlk - 1) / kBlk;
-    return ((size_t)num_seqs * 2 * nblk * sizeof(float) + 255) & ~(size_t)255;
+    return ((size_t)num_seqs * 2 * nblk * 3 * sizeof(uint64_t) + 255) & ~(size_t)255;
 }
 
 int ts_spec_accept(int32_t num_seqs, int32_t vocab, int32_t max_draft, const float *p_target,
@@ -392,7 +491,7 @@ int ts_spec_accept(int32_t num_seqs, int32_t vocab, int32_t max_draft, const flo
     a.u_sample = u_sample;
     a.n_accepted = num_accepted;
     a.next_token = next_token;
-    a.bsum = static_cast<float *>(workspace);
+    a.bsum = static_cast<uint64_t *>(workspace);
     a.B = num_seqs;
     a.V = vocab;
     a.G = max_draft;
