@@ -211,6 +211,14 @@ def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30, 
         except Exception as e:   # noqa: BLE001
             log(f"[bench] {name}: ceiling measurement failed: {e!r}")
             extra = dict(ceiling_error=repr(e))
+    # the output of one more call on pool 0 (the workload's own values) for
+    # the parity check against the oracle
+    k, v = pools[0]
+    binding.decode_attn(t["q"], k, v, t["page_table"], t["ctx_lens"], t["q_lens"], t["out"],
+                        wl.scale, workspace=ws, max_ctx_len=wl.max_ctx_len)
+    torch.cuda.synchronize()
+    from paper_2608_22788_amd import device
+    out_f64 = device.out_as_f64(t)
     # the memory stays in torch's cache for the next workload: memory obtained
     # from the driver again after a free streams up to 5 % slower here
     del pools, t, ws
@@ -220,62 +228,106 @@ def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30, 
                 kernel_ms_p10=float(np.percentile(kern_ms, 10)), kernel_ms_p90=float(np.percentile(kern_ms, 90)),
                 kv_gbps=kv / (ms_step * 1e-3) / 1e9,
                 kernel_gbps=alg / (kern_ms.mean() * 1e-3) / 1e9,
-                tokens_per_s=qtok / (ms_step * 1e-3), n_pools=n_pools, wl=wl, **extra)
+                query_tokens_per_s=qtok / (ms_step * 1e-3), tokens_per_s=wl.B / (ms_step * 1e-3),
+                n_pools=n_pools, wl=wl, out_f64=out_f64, **extra)
 
 
-def cpu_baseline(wl, min_seconds=10.0, max_runs=50):
-    """The float64 oracle on this host's cores over the whole bulk call,
-    repeated until about min_seconds of work (bounded by max_runs)."""
+def parity_errors(got, ref):
+    """Max-abs, mean-abs and relative L2 error over the valid output rows
+    (the oracle marks rows i >= q_lens[b] with NaN)."""
+    m = ~np.isnan(ref)
+    d = got[m] - ref[m]
+    return dict(max_abs=float(np.abs(d).max()), mean_abs=float(np.abs(d).mean()),
+                rel_l2=float(np.linalg.norm(d) / np.linalg.norm(ref[m])), elements=int(m.sum()),
+                finite=bool(np.isfinite(got[m]).all()))
+
+
+# Parity bar on bf16 outputs with N(0,1) inputs (max-abs, mean-abs), plus the
+# relative L2 bar that keeps the check meaningful at long context.
+PARITY_BAR = dict(max_abs=2e-2, mean_abs=2e-3, rel_l2=1e-2)
+
+
+def oracle_leg(r, threads, min_seconds=0.0, max_runs=50):
+    """The float64 oracle on this host's cores over the whole call of a timed
+    workload: its time per call (repeated for about min_seconds, bounded by
+    max_runs) and the parity of the GPU output of the same call."""
     import oracle
     orc = oracle.load()
-    log("[bench] cpu baseline: generating host inputs")
+    wl = r["wl"]
+    log(f"[bench] oracle {r['workload']}: generating host inputs")
     q, k, v = wl.q_values(), wl.k_pages(), wl.v_pages()
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
-    log(f"[bench] cpu baseline: oracle on {threads} threads")
-    runs, t0 = 0, time.perf_counter()
+    log(f"[bench] oracle {r['workload']}: {threads} threads")
+    runs, ref, t0 = 0, None, time.perf_counter()
     while runs < max_runs:
-        orc.attention(q, k, v, wl.page_table, wl.ctx_lens, wl.q_lens, wl.scale, nthreads=threads)
+        o = orc.attention(q, k, v, wl.page_table, wl.ctx_lens, wl.q_lens, wl.scale, nthreads=threads)
+        ref = o if ref is None else ref
         runs += 1
         if time.perf_counter() - t0 >= min_seconds:
             break
     dt = (time.perf_counter() - t0) / runs
+    del q, k, v
+    par = parity_errors(r["out_f64"], ref)
+    par["within_bar"] = par["finite"] and all(par[key] <= bar for key, bar in PARITY_BAR.items())
+    par = {key: (float(f"{val:.4g}") if isinstance(val, float) else val) for key, val in par.items()}
+    par["oracle_s"] = round(dt, 4)
+    return dt, runs, par
+
+
+def cpu_baseline(bulk, tails, min_seconds=10.0, max_runs=50):
+    """The float64 oracle on this host's cores over the whole bulk call,
+    repeated until about min_seconds of work (bounded by max_runs), then once
+    over each tail workload's whole call; every GPU output of those calls is
+    compared with it element by element."""
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    wl = bulk["wl"]
+    dt, runs, par_bulk = oracle_leg(bulk, threads, min_seconds, max_runs)
+    parity = {"bulk": par_bulk}
+    for name, r in tails.items():
+        if r is not None and "wl" in r:
+            parity[name] = oracle_leg(r, threads)[2]
     return dict(value=wl.kv_bytes() / dt / 1e9, unit="GB/s", cores=threads, kind="oracle",
                 sample=f"whole bulk call ({wl.B} seqs, {int(wl.ctx_lens.sum())} context tokens), "
                        f"float64, {runs} runs, {dt:.3f} s each",
                 seconds_per_call=round(dt, 4), os_cpu_count=os.cpu_count(),
-                omp_num_threads=os.environ.get("OMP_NUM_THREADS"))
+                omp_num_threads=os.environ.get("OMP_NUM_THREADS"),
+                parity=parity, parity_bar=PARITY_BAR,
+                parity_note="GPU output of one timed-configuration call per workload against the "
+                            "oracle over every sequence, row and head of that call")
 
 
-def makespan_model(sweep, wl):
+def makespan_model(decode_rows, wl):
     """The measured curve fed into the completion-time model (Sec. 2.1,
-    App. D): tau(b) = mean attention time per decoded position over the seeds,
-    tabulated for b = 1..512, then the bulk workload's lengths decoded on one
-    replica: its completion time and the share of the longest 5 % of requests."""
+    App. D) for the bulk pool, which decodes one token per step: tau(b) =
+    mean attention time per step over the seeds at q_len 1, tabulated for
+    b = 1..512, then the bulk workload's lengths decoded on one replica: its
+    completion time and the share of the longest 5 % of requests.  Only
+    q_len 1 points enter (verify points describe another regime)."""
     from paper_2608_22788_amd import binding
-    b = [r["batch"] for r in sweep]
-    tau = binding.tau_table(b, [r["tau_us"] for r in sweep], max(b))
+    rows = sorted((r for r in decode_rows if r["q_len"] == 1), key=lambda r: r["batch"])
+    b = [r["batch"] for r in rows]
+    tau = binding.tau_table(b, [r["tau_us"] for r in rows], max(b))
     L = wl.ctx_lens.astype(np.int64)
     T = binding.replica_time(tau, L)
     sh = binding.request_shares(tau, L)
     top = np.argsort(L)[::-1][:max(1, len(L) // 20)]
-    return dict(tau_source="sweep mean tau_us per batch size", bmax=max(b),
-                bulk_requests=len(L), bulk_replica_attention_s=round(T / 1e6, 6),
+    return dict(tau_source="mean call time per batch size at q_len 1 (sweep points with q_len 1, "
+                           "plus a q_len 1 run of the sweep at the batch sizes it verifies at)",
+                batches=b, bmax=max(b), bulk_requests=len(L), bulk_replica_attention_s=round(T / 1e6, 6),
                 longest_5pct_share=round(float(sh[top].sum() / T), 4))
 
 
 def depth_sweep(depths=(1, 2, 3, 4, 5, 6), seed_count=1):
     """Route-specialised speculative decoding (Sec. 3.4, Sec. 4.3): the same
     concurrency sweep with every batch size verifying q_len = 1 + gamma
-    tokens per sequence.  tau_us (call time / q_len) is the attention time per
-    drafted position if every draft is accepted."""
+    tokens per sequence; the median call time per step.  How many tokens a
+    step emits depends on acceptance, which is not modelled here."""
     from paper_2608_22788_amd import binding
     rows = []
     for q in depths:
-        pts = binding.concurrency_sweep(seeds=seed_count, warmup=10, iters=20, verify_max_batch=4096,
-                                        verify_q_len=q)
+        pts = binding.concurrency_sweep(seeds=seed_count, warmup=10, iters=20,
+                                        verify_max_batch=4096 if q > 1 else 0, verify_q_len=max(q, 1))
         for r in sweep_summary(pts):
-            rows.append(dict(q_len=q, batch=r["batch"], kv_gbps=r["kv_gbps"], call_us=round(r["tau_us"] * q, 2),
-                             tau_us=r["tau_us"]))
+            rows.append(dict(q_len=q, batch=r["batch"], kv_gbps=r["kv_gbps"], call_us=r["call_us"]))
     return rows
 
 
@@ -436,11 +488,21 @@ def spec_step(steps=50, vocab=151936):
 
 
 def sweep_summary(points):
-    """Per batch size: mean, min and max over seeds of the sweep figures."""
+    """Per batch size: mean, min and max over seeds of the sweep figures.
+    call_us is the median time of one step; tokens_per_s and tau_us count one
+    emitted token per sequence and step (a verify step's accepted drafts are
+    not credited), so at q_len > 1 they are a floor."""
     out = []
     for b in sorted({p["batch"] for p in points}):
         ps = [p for p in points if p["batch"] == b]
-        row = dict(batch=b, q_len=ps[0]["q_len"], seeds=len(ps))
+        q = ps[0]["q_len"]
+        row = dict(batch=b, q_len=q, seeds=len(ps),
+                   regime="decode (one query token per sequence)" if q == 1 else
+                   f"verify ({q} query tokens per sequence, one emitted token per step credited)")
+        calls = np.array([p["t_median_us"] for p in ps])
+        row["call_us"] = round(float(calls.mean()), 2)
+        row["call_us_min"] = round(float(calls.min()), 2)
+        row["call_us_max"] = round(float(calls.max()), 2)
         for f, nd in (("kv_gbps", 1), ("hbm_frac", 4), ("tokens_per_s", 0), ("tau_us", 2)):
             xs = np.array([p[f] for p in ps])
             row[f] = round(float(xs.mean()), nd)
@@ -516,7 +578,7 @@ def main():
             torch.cuda.synchronize()
             del src, dst
         r = time_workload(args.only, args.steps, args.warmup, MIN_WARMUP_MS, ceiling=not args.no_ceiling)
-        r.pop("wl")
+        r.pop("wl"), r.pop("out_f64")
         print(json.dumps(r), flush=True)
         return
 
@@ -532,10 +594,13 @@ def main():
             traceback.print_exc(file=sys.stderr)
             return {"error": repr(e)}
 
+    tail_runs = {}
+
     def tail_one(name):
         r = time_workload(name, args.steps, args.warmup, MIN_WARMUP_MS, ceiling=not args.no_ceiling)
-        r.pop("wl")
-        out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
+        tail_runs[name] = r
+        out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()
+               if k not in ("wl", "out_f64")}
         out["hbm_frac"] = round(r["kv_gbps"] / PEAK_GBPS, 4)
         out["kernel"] = KERNELS[name]
         out["kernel_frac"] = round(r["kernel_gbps"] / PEAK_GBPS, 4)
@@ -559,7 +624,7 @@ def main():
                 cfg = dict(synth.CONFIGS["bulk"], Hq=Hq, Hkv=Hkv, q_len=ql)
                 r = time_workload(key, args.steps, args.warmup, MIN_WARMUP_MS, ceiling=not args.no_ceiling,
                                   cfg=cfg)
-                r.pop("wl")
+                r.pop("wl"), r.pop("out_f64")
                 out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
                 out["heads"] = f"{Hq} q / {Hkv} kv"
                 out["q_len"] = ql
@@ -576,7 +641,7 @@ def main():
             def shard_one(parent=parent):
                 r = time_workload(parent + "_tp2", args.steps, args.warmup, MIN_WARMUP_MS,
                                   ceiling=not args.no_ceiling, cfg=tp2_share(parent))
-                r.pop("wl")
+                r.pop("wl"), r.pop("out_f64")
                 out = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in r.items()}
                 out["heads"] = "16 q / 4 kv"
                 out["hbm_frac"] = round(r["kv_gbps"] / PEAK_GBPS, 4)
@@ -585,13 +650,19 @@ def main():
                 return out
             shards[parent + "_tp2"] = guarded(parent + " tp2 share", shard_one)
     sweep = []
+    decode_small = None
     model = None
     if not args.no_sweep:
         log(f"[bench] concurrency sweep ({args.sweep_seeds} seeds)")
         sweep = guarded("sweep", lambda: sweep_summary(
-            binding.concurrency_sweep(seeds=args.sweep_seeds, warmup=20, iters=30)))
-        if isinstance(sweep, list):
-            model = guarded("makespan model", lambda: makespan_model(sweep, bulk["wl"]))
+            binding.concurrency_sweep(seeds=args.sweep_seeds, warmup=20, iters=100)))
+        # the batch sizes the sweep verifies at, decoding one token instead:
+        # with the sweep's q_len 1 points this is the bulk pool's tau(b)
+        decode_small = guarded("decode sweep", lambda: sweep_summary(
+            binding.concurrency_sweep(batches=(1, 2, 4, 8), seeds=args.sweep_seeds, warmup=20, iters=100,
+                                      verify_max_batch=0)))
+        if isinstance(sweep, list) and isinstance(decode_small, list):
+            model = guarded("makespan model", lambda: makespan_model(sweep + decode_small, bulk["wl"]))
     mixed = None
     if not args.no_mixed:
         log("[bench] ragged mixed batch and graph replay")
@@ -604,7 +675,7 @@ def main():
     if not args.no_depth_sweep:
         log("[bench] draft-depth sweep (q_len 1..6 at every batch size, seed 0)")
         depth = guarded("depth sweep", depth_sweep)
-    cpu = None if args.no_cpu_baseline else guarded("cpu baseline", lambda: cpu_baseline(bulk["wl"]))
+    cpu = None if args.no_cpu_baseline else guarded("cpu baseline", lambda: cpu_baseline(bulk, tail_runs))
 
     achieved = bulk["kernel_gbps"]
     if cpu and "value" in cpu:
@@ -628,6 +699,7 @@ def main():
                    "parallelism": "single GPU"},
         "hbm_frac": round(bulk["kv_gbps"] / PEAK_GBPS, 4),
         "tokens_per_s": round(bulk["tokens_per_s"]),
+        "parity": cpu.get("parity") if isinstance(cpu, dict) else None,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_GBPS, 4), "traffic": traffic,
                      "kernel": KERNELS["bulk"],
@@ -646,6 +718,7 @@ def main():
         "tp2_shares": shards,
         "group_sizes": groups,
         "sweep": sweep,
+        "sweep_decode_small_batches": decode_small if not args.no_sweep else None,
         "makespan_model": model,
         "mixed_batch": mixed,
         "spec_step": spec,

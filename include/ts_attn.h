@@ -35,22 +35,20 @@
  * library allocates nothing inside ts_decode_attn, never synchronises it and
  * never reads device data on the host, so a call can be captured into a HIP
  * graph.  Inputs are read-only; out is written only at rows i < q_lens[b]
- * (q_lens[b] = 0 skips sequence b).  The workspace starts with a fixed
- * 1 MiB area of arrival counters (one per (sequence, KV head)), followed by
- * split partial results.  It must be zero-filled before its first use (e.g.
- * hipMemset once after allocation); every completed call leaves the counters
- * zero again and never writes partial results over them, so a workspace can
- * be reused by any later call, of any shape, on one stream.  Calls that may
- * run concurrently need distinct workspaces.  Every entry point
+ * (q_lens[b] = 0 skips sequence b).  The workspace holds split partial
+ * results, the arrival counters of the in-kernel combine (cleared by the call
+ * itself) and the TS_DEBUG flag word; it needs no initialisation, its contents
+ * are undefined on return, and a workspace can be reused by any later call,
+ * of any shape, on one stream.  Calls that may run concurrently need distinct
+ * workspaces.  Every entry point
  * returns TS_OK (0) or a negative ts_status; on error nothing is launched and
  * ts_last_error() describes the cause.  No C++ exception crosses the ABI.
  *
  * Device-side preconditions (1 <= q_lens[b] <= ctx_lens[b] <= max_ctx_len,
  * ctx_lens[b] <= max_pages_per_seq * page_size, q_lens[b] <= max_q_len, page
  * ids in [0, num_pages)) are the caller's to keep on the fast path; with the
- * environment variable TS_DEBUG=1 a checking kernel verifies them (and that
- * the workspace counters are zero) first, the call synchronises and returns
- * TS_ERR_SHAPE (TS_ERR_WORKSPACE for the counters) if any fails.
+ * environment variable TS_DEBUG=1 a checking kernel verifies them first, the
+ * call synchronises and returns TS_ERR_SHAPE if any fails.
  */
 #ifndef TS_ATTN_H
 #define TS_ATTN_H
@@ -62,7 +60,7 @@
 extern "C" {
 #endif
 
-#define TS_ATTN_ABI_VERSION 2
+#define TS_ATTN_ABI_VERSION 3
 
 typedef enum ts_status {
     TS_OK = 0,
@@ -113,15 +111,16 @@ typedef struct ts_attn_shape {
 } ts_attn_shape;
 
 /* Bytes of device workspace ts_decode_attn needs for this shape (split-KV
- * partial outputs, their log-sum-exp and the per-unit arrival counters).
+ * partial outputs, their log-sum-exp, the per-unit arrival counters and the
+ * TS_DEBUG flag word).
  * Host only; returns 0 and sets ts_last_error() for an unsupported shape. */
 size_t ts_decode_attn_workspace_size(const ts_attn_shape *shape);
 
 /* Paged decode / verify attention as defined above, enqueued on `stream`
  * (a hipStream_t; NULL is the default stream).  `scale` multiplies the dot
  * products (typically 1/sqrt(head_dim)).  `workspace` is device memory of at
- * least ts_decode_attn_workspace_size(shape) bytes, 256-byte aligned,
- * zero-filled before its first use (see above). */
+ * least ts_decode_attn_workspace_size(shape) bytes, 256-byte aligned, with
+ * any contents. */
 int ts_decode_attn(const ts_attn_shape *shape, const void *q, const void *k_pages,
                    const void *v_pages, const int32_t *page_table, const int32_t *ctx_lens,
                    const int32_t *q_lens, void *out, float scale, void *workspace,
@@ -160,6 +159,10 @@ typedef struct ts_sweep_config {
     int32_t warmup;             /* untimed calls per point */
     int32_t iters;              /* timed calls per point */
     int64_t min_rotation_bytes; /* KV bytes cycled through per point (>= 1 GiB) */
+    double verify_tokens_per_step; /* tokens a verify step emits per sequence (accepted
+                                      drafts + 1); the sweep does not model acceptance,
+                                      so the caller states it; <= 0 reads as 1.  A
+                                      one-token decode step emits 1. */
 } ts_sweep_config;
 
 typedef struct ts_sweep_point {
@@ -174,8 +177,10 @@ typedef struct ts_sweep_point {
     double t_p90_us;
     double kv_gbps;             /* kv_bytes / t_median */
     double hbm_frac;            /* kv_gbps / 8000 (MI355X HBM3E peak) */
-    double tokens_per_s;        /* batch * q_len / t_median */
-    double tau_us;              /* t_median / q_len: attention time per decoded position */
+    double tokens_per_s;        /* batch * tokens per step / t_median (tokens per step: 1
+                                   at q_len 1, verify_tokens_per_step when verifying) */
+    double tau_us;              /* t_median / tokens per step: attention time per emitted
+                                   token of one sequence, the attention share of tau(b) */
     double gather_median_us;    /* per-call time of ts_page_gather_read over the same pools
                                    (the read-only floor of the same call) */
 } ts_sweep_point;

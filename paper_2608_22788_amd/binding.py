@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(HERE, "libtsattn.so")
 # TS_ATTN_ABI_VERSION of the header these structures mirror: a library built
 # from another version may lay its structures out differently, so loading
 # one is refused.
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 TS_OK = 0
 STATUS = {0: "TS_OK", -1: "TS_ERR_NULL", -2: "TS_ERR_SHAPE", -3: "TS_ERR_WORKSPACE",
@@ -45,7 +45,7 @@ class SweepConfig(ctypes.Structure):
                 ("batches", ctypes.c_int32 * 32), ("verify_max_batch", ctypes.c_int32),
                 ("verify_q_len", ctypes.c_int32), ("num_seeds", ctypes.c_int32),
                 ("warmup", ctypes.c_int32), ("iters", ctypes.c_int32),
-                ("min_rotation_bytes", ctypes.c_int64)]
+                ("min_rotation_bytes", ctypes.c_int64), ("verify_tokens_per_step", ctypes.c_double)]
 
 
 class SweepPoint(ctypes.Structure):
@@ -191,10 +191,11 @@ def _check_tensors(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out):
 
 
 def new_workspace(nbytes: int, device="cuda"):
-    """A zero-filled workspace of nbytes (the library requires zeros before
-    the first use and leaves its split counters zero after every call)."""
+    """A workspace of nbytes.  The library needs no particular contents, so
+    it is filled with a non-zero byte pattern: every caller then exercises
+    that contract."""
     import torch
-    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
+    return torch.full((nbytes,), 0xA7, dtype=torch.uint8, device=device)
 
 
 def decode_attn(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale: float,
@@ -312,7 +313,7 @@ def concurrency_sweep(batches: Sequence[int] = (1, 2, 4, 8, 16, 32, 64, 128, 256
                       seeds: int = 5, warmup: int = 5, iters: int = 50,
                       num_q_heads: int = 32, num_kv_heads: int = 8, head_dim: int = 128,
                       verify_max_batch: int = 8, verify_q_len: int = 4,
-                      min_rotation_bytes: int = 1 << 30) -> List[dict]:
+                      min_rotation_bytes: int = 1 << 30, verify_tokens_per_step: float = 1.0) -> List[dict]:
     cfg = SweepConfig()
     cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim = num_q_heads, num_kv_heads, head_dim
     cfg.num_batches = len(batches)
@@ -321,6 +322,7 @@ def concurrency_sweep(batches: Sequence[int] = (1, 2, 4, 8, 16, 32, 64, 128, 256
     cfg.verify_max_batch, cfg.verify_q_len = verify_max_batch, verify_q_len
     cfg.num_seeds, cfg.warmup, cfg.iters = seeds, warmup, iters
     cfg.min_rotation_bytes = min_rotation_bytes
+    cfg.verify_tokens_per_step = verify_tokens_per_step
     cap = len(batches) * seeds
     pts = (SweepPoint * cap)()
     n = ctypes.c_int32()

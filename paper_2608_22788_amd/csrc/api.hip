@@ -24,8 +24,9 @@ kernel_fn decode_q1_variant(int D, int G);
 kernel_fn verify_variant(int D, int NB);
 kernel_fn verify_team_variant(int rows, int *lds_bytes, int *nbe);
 kernel_fn merge_variant(int D, bool few);
+void (*clear_counters_fn())(int *, int);
 int debug_check(const ts_attn_shape *s, const int32_t *page_table, const int32_t *ctx_lens,
-                const int32_t *q_lens, const int *counters, hipStream_t stream);
+                const int32_t *q_lens, int *flags, hipStream_t stream);
 
 static thread_local std::string g_last_error;
 
@@ -76,7 +77,7 @@ struct Plan {
     bool team;        // verify by four-wavefront teams sharing pages in LDS (head_dim 128)
     bool auto_w;      // worker count chosen by the library (W is then an upper bound)
     int G, NB, rows_per_unit, W;
-    size_t ws_cnt_off, ws_o_off, ws_lse_off, ws_bytes;
+    size_t ws_cnt_off, ws_dbg_off, ws_o_off, ws_lse_off, ws_bytes;
 };
 
 // Number of workers sharing the KV stream.  MI355X has 256 compute units.
@@ -197,12 +198,13 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
                (s->variant == TS_VARIANT_TEAM || (s->variant == TS_VARIANT_AUTO && pl->NB >= 3));
     pl->auto_w = s->num_workers == 0;
     pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team, pl->rows_per_unit);
-    // Workspace: the split counters first, at a fixed size whatever the shape,
-    // so that no call's partial results ever land on them; then the partial
-    // outputs and their log-sum-exp.
+    // Workspace: the split counters first (one per unit, cleared by each call
+    // that uses them), then 256 bytes for the TS_DEBUG check's flag word, then
+    // the partial outputs and their log-sum-exp.
     const size_t slots = 2 * (size_t)pl->W;
     pl->ws_cnt_off = 0;
-    pl->ws_o_off = kCounterBytes;
+    pl->ws_dbg_off = kCounterBytes;
+    pl->ws_o_off = pl->ws_dbg_off + 256;
     const size_t o_bytes = slots * pl->rows_per_unit * s->head_dim * sizeof(float);
     pl->ws_lse_off = pl->ws_o_off + ((o_bytes + 255) & ~(size_t)255);
     pl->ws_bytes = pl->ws_lse_off + ((slots * pl->rows_per_unit * sizeof(float) + 255) & ~(size_t)255);
@@ -245,7 +247,8 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
 
     int *counters = reinterpret_cast<int *>(static_cast<char *>(workspace) + pl.ws_cnt_off);
     if (debug_enabled()) {
-        st = debug_check(s, page_table, ctx_lens, q_lens, counters, hs);
+        int *flags = reinterpret_cast<int *>(static_cast<char *>(workspace) + pl.ws_dbg_off);
+        st = debug_check(s, page_table, ctx_lens, q_lens, flags, hs);
         if (st)
             return st;
     }
@@ -303,6 +306,13 @@ static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, co
     p.fuse_splits = !pl.team && (int64_t)p.B * p.Hkv >= 2 * (int64_t)p.W;
 
     hipError_t e;
+    if (p.fuse_splits) {
+        // the arrival counters of this call's units start at zero
+        const int n = p.B * p.Hkv;
+        hipLaunchKernelGGL(clear_counters_fn(), dim3((n + 255) / 256), dim3(256), 0, hs, counters, n);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return hip_fail(e, "counter clear launch");
+    }
     if (ev_begin || ev_end) {
         // the events take the kernel's own start and end timestamps
         void *args[] = {&p};

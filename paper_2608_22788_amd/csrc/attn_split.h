@@ -21,27 +21,31 @@ namespace tsattn {
 constexpr int kMergeBatch = 8;
 
 // Loads and stores coherent across the whole device (the L2 caches of all
-// XCDs): on gfx950 these are the device-scope cache-policy forms of plain
-// global loads and stores, and a store is visible device-wide once the
-// issuing wavefront's vector memory counter has drained.
+// XCDs): relaxed atomics at agent scope, which on gfx950 are plain global
+// loads and stores with the device-scope cache policy.  A store is visible
+// device-wide once the issuing wavefront's vector memory counter has drained.
 __device__ __forceinline__ float ld_coherent(const float *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void st_coherent(float *p, float v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// 16-byte form of st_coherent (p 16-byte aligned).  The device-scope policy
-// bit is only reachable for vector stores through an instruction written out.
-// A store of more than 8 bytes still reads its data registers for a moment
-// after it issues, and the compiler does not see inside the instruction to
-// protect them (it reused them at once and corrupted partial rows), so two
-// wait states follow it.  wait_vmem() below covers the store's completion.
+// 16 bytes (p 16-byte aligned) as two 8-byte device-scope stores.
 __device__ __forceinline__ void st_coherent16(float *p, f32x4_t v) {
-    asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" : : "v"(p), "v"(v) : "memory");
+    uint64_t *q = reinterpret_cast<uint64_t *>(p);
+    const f32x2_t lo = {v[0], v[1]}, hi = {v[2], v[3]};
+    __hip_atomic_store(q, __builtin_bit_cast(uint64_t, lo), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(q + 1, __builtin_bit_cast(uint64_t, hi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// Waits until every vector memory operation this wavefront issued is complete.
+// Waits until every vector memory operation this wavefront issued is
+// complete.  The wait itself is not a memory operation to the compiler, so
+// compiler-only fences on both sides keep every memory access written before
+// it above it and every one written after it below it (they emit no
+// instruction; no cache is written back or invalidated).
 __device__ __forceinline__ void wait_vmem() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0); expcnt, lgkmcnt left at their maximum
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // The workers whose ranges meet the unit that occupies global pages
@@ -183,8 +187,7 @@ __device__ __forceinline__ void write_merged(const AttnParams &p, int b, int g, 
 
 // Combines all pieces of unit (b, g) and writes its rows (one wavefront;
 // rows_per_unit rows, 4 per pass; rows of draft positions >= q_len are
-// skipped).  Called by the worker that counted the last arrival on the unit,
-// which then sets the counter back to zero for the next call.
+// skipped).  Called by the worker that counted the last arrival on the unit.
 template <int D>
 __device__ void combine_unit(const AttnParams &p, int b, int g, const UnitSplit &u, int lane) {
     const int part = lane & 15;
@@ -199,14 +202,14 @@ __device__ void combine_unit(const AttnParams &p, int b, int g, const UnitSplit 
         if (row_ok)
             write_merged<D>(p, b, g, r, part, a);
     }
-    __hip_atomic_store(p.counters + (size_t)b * p.Hkv + g, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Counts this wavefront's arrival on the unit of a piece whose partial it has
 // just written with device-coherent stores; the last arriver combines the
 // unit.  The stores are complete once the vector memory counter has drained,
 // so no cache-wide fence is needed, and the last arriver's loads are issued
-// after its count returned.
+// after its count returned.  The counters start at zero: the call clears
+// them before the streaming kernel runs.
 template <int D>
 __device__ void arrive_and_combine(const AttnParams &p, const Segment &s, int64_t ptot, int lane) {
     wait_vmem();

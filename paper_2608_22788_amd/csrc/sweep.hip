@@ -204,8 +204,13 @@ int run_point(const ts_sweep_config &c, const Point &P, Arena &A, hipStream_t st
     pt->t_p90_us = quantile(us, 0.9);
     pt->kv_gbps = (double)pt->kv_bytes / (pt->t_median_us * 1e-6) / 1e9;
     pt->hbm_frac = pt->kv_gbps / 8000.0;
-    pt->tokens_per_s = (double)batch * Q / (pt->t_median_us * 1e-6);
-    pt->tau_us = pt->t_median_us / Q;
+    // Tokens emitted per sequence and step: one for plain decode; a verify
+    // step emits its accepted drafts plus one, which the caller states
+    // (acceptance is not modelled here), so drafts are never counted as
+    // emitted tokens by default.
+    const double per_step = (Q > 1 && c.verify_tokens_per_step > 0.0) ? c.verify_tokens_per_step : 1.0;
+    pt->tokens_per_s = (double)batch * per_step / (pt->t_median_us * 1e-6);
+    pt->tau_us = pt->t_median_us / per_step;
     pt->gather_median_us = quantile(gus, 0.5);
     return TS_OK;
 }

@@ -29,7 +29,7 @@ def test_exports_every_declared_function():
 
 
 def test_version_and_status_strings():
-    assert b.lib.ts_version() == b.ABI_VERSION == 2
+    assert b.lib.ts_version() == b.ABI_VERSION == 3
     for st in (0, -1, -2, -3, -4, -5, -6):
         assert b.lib.ts_status_string(st)
     assert b.lib.ts_status_string(-99) == b"unknown status"

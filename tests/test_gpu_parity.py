@@ -1,9 +1,14 @@
 """Parity of the HIP path (through the C ABI) with the float64 oracle.
 
-Small cases compare every output element; the full-size workloads compare
-every row of sampled sequences (the longest, the shortest and random others)
-computed in the same launch configuration the benchmark times, plus
-properties that hold at any size (finite outputs, untouched canaries)."""
+Every test compares every output element of the call it makes: the small
+and random cases, and the full-size workloads (bulk, MTP verify, block-draft
+verify and every seed-0 point of the concurrency sweep) in the launch
+configuration the benchmark times.  The oracle sees the host generator's
+values; the GPU sees the library's device fill of the same definition,
+checked bit for bit against the host side.  Properties that hold at any
+size are checked too (finite outputs, untouched canaries).  A few side
+cases (group sizes, TP2 shares, the ragged mixed batch) compare sampled
+sequences."""
 import numpy as np
 import pytest
 
@@ -149,17 +154,18 @@ def test_many_sequences(dev, orc, B, Qmax):
 
 
 def test_workspace_reused_across_calls_and_shapes(dev, orc):
-    """One zero-filled workspace serves a run of calls of different shapes and
-    worker counts; each result matches the oracle, and after every call the
-    per-unit arrival counters (the first B * Hkv int32 of the workspace) are
-    zero again."""
+    """One workspace serves a run of calls of different shapes and worker
+    counts; it starts full of non-zero bytes and is overwritten with random
+    bytes between calls (the library needs no particular contents), and each
+    result matches the oracle."""
     import torch
     from paper_2608_22788_amd import binding
     _, device = dev
-    ws = binding.new_workspace(64 << 20)
+    ws = torch.full((64 << 20,), 0xFF, dtype=torch.uint8, device="cuda")
     cases = [(32, 8, 128, [1] * 5, [1, 15, 16, 33, 1000], 0), (8, 2, 64, [1] * 3, [16, 17, 300], 3),
              (32, 8, 128, [4, 4], [500, 77], 0), (32, 8, 128, [1] * 40, [130] * 40, 300),
-             (16, 2, 128, [1, 1, 1], [64, 65, 511], 1)]
+             (16, 2, 128, [1, 1, 1], [64, 65, 511], 1), (32, 8, 128, [1] * 256, [40] * 256, 0)]
+    gen = torch.Generator(device="cuda").manual_seed(5)
     for n, (Hq, Hkv, D, ql, cl, w) in enumerate(cases):
         wl = synth.make_workload(f"reuse{n}", seed=40 + n, cfg=small_cfg(Hq, Hkv, D), ctx_lens=cl, q_lens=ql)
         ref = oracle_out(orc, wl)
@@ -167,8 +173,7 @@ def test_workspace_reused_across_calls_and_shapes(dev, orc):
         say(f"reuse case {n}: B={wl.B} Hq={Hq} Hkv={Hkv} D={D} workers={w}")
         device.run(wl, t, num_workers=w, workspace=ws)
         assert_parity(device.out_as_f64(t), ref, f"reuse{n}")
-        torch.cuda.synchronize()
-        assert int(ws[:1 << 20].count_nonzero()) == 0, f"counters left set after case {n}"
+        ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, device="cuda", generator=gen))
 
 
 @pytest.mark.parametrize("Qmax", [1, 4])
@@ -181,8 +186,7 @@ def test_in_kernel_combine_with_many_pieces(dev, orc, Qmax):
     q = [Qmax] * 100
     wl = synth.make_workload("manypieces", seed=21, cfg=small_cfg(32, 8, 128), ctx_lens=ctx, q_lens=q,
                              poison=True, spare_pages=1)
-    seqs = [0, 1, 50, 99]
-    ref = oracle_out(orc, wl.subset(seqs))
+    ref = oracle_out(orc, wl)
     t = device.upload(wl)
     for var in (0, 1, 3) if Qmax == 1 else (0, 1):
         for w in (300, 397):
@@ -191,7 +195,7 @@ def test_in_kernel_combine_with_many_pieces(dev, orc, Qmax):
             device.run(wl, t, num_workers=w, variant=var)
             got = device.out_as_f64(t)
             canary_ok(t, wl)
-            assert_parity(got[seqs], ref, f"manypieces v{var} w{w}")
+            assert_parity(got, ref, f"manypieces v{var} w{w}")
 
 
 def test_no_work_at_all():
@@ -305,7 +309,7 @@ def test_split_points_do_not_change_the_result(dev):
 
 
 # ---------------------------------------------------------------------------
-# full-size workloads, sampled against the oracle
+# full-size workloads against the oracle
 # ---------------------------------------------------------------------------
 
 FULL = {"bulk": 6, "mtp": 3, "dflash": 2}
@@ -313,20 +317,26 @@ FULL = {"bulk": 6, "mtp": 3, "dflash": 2}
 
 @pytest.mark.parametrize("name", list(FULL))
 def test_full_size_config(dev, orc, name):
+    """The benchmarked workloads in full: every sequence, row and head of the
+    call against the oracle, for the automatic launch (the one the benchmark
+    times) and every other kernel variant."""
     _, device = dev
     wl = synth.make_workload(name, seed=0)
     say(f"full {name}: B={wl.B} sum_ctx={int(wl.ctx_lens.sum())} max={wl.max_ctx_len} "
         f"KV={wl.kv_bytes() / 1e9:.2f} GB")
     t = device.upload(wl, values="device")
-    seqs = sample_seqs(wl, FULL[name])
-    ref = oracle_out(orc, wl.subset(seqs))
+    say(f"  oracle over the whole call (host inputs)")
+    ref = oracle_out(orc, wl)
     for var in variants_for(wl):
         t["out_full"].fill_(device.CANARY)
         device.run(wl, t, variant=var)      # variant 0 / auto is the benchmarked launch
         got = device.out_as_f64(t)
         canary_ok(t, wl)
-        assert np.isfinite(got).all()
-        assert_parity(got[seqs], ref, f"{name} seqs {seqs} variant {var}")
+        assert np.isfinite(got[~np.isnan(ref)]).all()
+        assert_parity(got, ref, f"{name} all {wl.B} seqs variant {var}")
+        # and no sequence is far off while the whole stays inside the bar
+        worst = max(float(np.nanmax(np.abs(got[b] - ref[b]))) for b in range(wl.B))
+        assert worst <= 2e-2, f"{name} variant {var}: a sequence has max_abs {worst:g}"
 
 
 @pytest.mark.parametrize("name", ["bulk", "dflash"])
@@ -374,8 +384,8 @@ def test_full_size_group_sizes(dev, orc, Hq, Hkv, ql):
 def test_full_size_ragged_mixed_batch(dev, orc):
     """One launch over the bulk workload in which the 8 longest sequences
     verify 4 drafted tokens and the other 248 decode one (ragged q_lens under
-    max_q_len 4), the benchmark's mixed-batch case; sampled rows of both kinds
-    against the oracle, padded rows untouched."""
+    max_q_len 4), the benchmark's mixed-batch case; rows of both kinds
+    against the oracle (every sequence), padded rows untouched."""
     _, device = dev
     base = synth.make_workload("bulk", seed=0)
     tail = np.argsort(base.ctx_lens)[::-1][:8]
@@ -383,14 +393,13 @@ def test_full_size_ragged_mixed_batch(dev, orc):
     ql[tail] = 4
     wl = synth.make_workload("bulk", seed=0, q_lens=ql.tolist(), Qmax=4)
     t = device.upload(wl, values="device")
-    seqs = sorted(set(sample_seqs(wl, 4)) | {int(tail[0]), int(tail[5])})
-    ref = oracle_out(orc, wl.subset(seqs))
+    ref = oracle_out(orc, wl)
     for var in variants_for(wl):
         t["out_full"].fill_(device.CANARY)
         device.run(wl, t, variant=var)
         got = device.out_as_f64(t)
         canary_ok(t, wl)
-        assert_parity(got[seqs], ref, f"mixed seqs {seqs} variant {var}")
+        assert_parity(got, ref, f"mixed all seqs variant {var}")
 
 
 SWEEP_CASES = [(b, 0) for b in synth.SWEEP_BATCHES] + \
@@ -399,6 +408,8 @@ SWEEP_CASES = [(b, 0) for b in synth.SWEEP_BATCHES] + \
 
 @pytest.mark.parametrize("batch,seed", SWEEP_CASES)
 def test_sweep_workload(dev, orc, batch, seed):
+    """Every sweep point of seed 0, and of seeds 1-4 up to 64 sequences, in
+    full against the oracle."""
     _, device = dev
     wl = synth.make_workload(f"sweep_b{batch}", seed=seed)
     say(f"sweep b={batch} seed={seed}: q_len={wl.Qmax} sum_ctx={int(wl.ctx_lens.sum())}")
@@ -407,9 +418,8 @@ def test_sweep_workload(dev, orc, batch, seed):
     got = device.out_as_f64(t)
     canary_ok(t, wl)
     assert np.isfinite(got).all()
-    seqs = sample_seqs(wl, 3 if batch > 8 else batch, seed)
-    ref = oracle_out(orc, wl.subset(seqs))
-    assert_parity(got[seqs], ref, f"sweep b{batch} s{seed}")
+    ref = oracle_out(orc, wl)
+    assert_parity(got, ref, f"sweep b{batch} s{seed} all seqs")
 
 
 def test_concurrency_sweep_entry_point(dev):
