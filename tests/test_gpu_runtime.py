@@ -78,6 +78,9 @@ DEBUG_SCRIPT = textwrap.dedent("""
         results.append(str(e.status) + ":" + str(e))
     # a workspace of arbitrary bytes passes the check, gives the result of a
     # fresh one, and the failed checks above left no flag behind in it
+    fresh = torch.zeros((8 << 20,), dtype=torch.uint8, device="cuda")
+    device.run(wl, t, num_workers=7, workspace=fresh)
+    torch.cuda.synchronize()
     ref = t["out"].clone()
     dirty = torch.full((8 << 20,), 0xFF, dtype=torch.uint8, device="cuda")
     for _ in range(2):
