@@ -136,6 +136,24 @@ int ts_decode_attn_events(const ts_attn_shape *shape, const void *q, const void 
                           float scale, void *workspace, size_t workspace_bytes, void *stream,
                           void *ev_begin, void *ev_end);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * ts_decode_attn with the same arguments but no workspace.  Its split
+ * partials, arrival counters and TS_DEBUG flag word live in a static device
+ * array of TS_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds
+ * until the process ends.  The call allocates nothing, on the host's HIP
+ * runtime or elsewhere.  Shapes whose ts_decode_attn_workspace_size exceeds
+ * the array are rejected with TS_ERR_WORKSPACE before anything is launched
+ * (every shape with num_workers = 0 fits).  Every call on one GPU shares that
+ * GPU's array, so calls that may overlap on one GPU (different streams, or
+ * graphs replayed concurrently) race and must not be issued; the call clears
+ * what it needs zeroed itself. */
+#define TS_NOALLOC_SCRATCH_BYTES ((size_t)48 << 20)
+
+int ts_decode_attn_noalloc(const ts_attn_shape *shape, const void *q, const void *k_pages,
+                           const void *v_pages, const int32_t *page_table, const int32_t *ctx_lens,
+                           const int32_t *q_lens, void *out, float scale, void *stream);
+
 /* ---- concurrency-throughput curve ------------------------------------------
  * The paper's controller consumes a measured decode throughput v(b) versus
  * active batch b, and the per-token time tau(b) = 1 / v(b) (Sec. 2.1;

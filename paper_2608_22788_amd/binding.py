@@ -58,7 +58,7 @@ class SweepPoint(ctypes.Structure):
                 ("gather_median_us", ctypes.c_double)]
 
 
-EXPORTS = ["ts_decode_attn_workspace_size", "ts_decode_attn", "ts_decode_attn_events",
+EXPORTS = ["ts_decode_attn_workspace_size", "ts_decode_attn", "ts_decode_attn_events", "ts_decode_attn_noalloc",
            "ts_concurrency_sweep", "ts_synth_fill_bf16", "ts_synth_sweep_lengths",
            "ts_synth_page_table", "ts_copy_bytes", "ts_stream_read", "ts_page_gather_read", "ts_event_create", "ts_event_destroy",
            "ts_event_record", "ts_event_elapsed_ms", "ts_status_string", "ts_last_error",
@@ -117,6 +117,8 @@ def _load() -> ctypes.CDLL:
     lib.ts_request_shares.restype = ctypes.c_int
     lib.ts_step_makespan.argtypes = [P, I32, P, P, I32, I32, P, ctypes.POINTER(ctypes.c_double)]
     lib.ts_step_makespan.restype = ctypes.c_int
+    lib.ts_decode_attn_noalloc.argtypes = [pshape, P, P, P, P, P, P, P, ctypes.c_float, P]
+    lib.ts_decode_attn_noalloc.restype = ctypes.c_int
     lib.ts_kv_append.argtypes = [pshape, P, P, P, P, P, P, P, P]
     lib.ts_kv_append.restype = ctypes.c_int
     lib.ts_spec_accept_workspace_size.argtypes = [I32, I32]
@@ -223,6 +225,19 @@ def decode_attn(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale: f
     else:
         check(lib.ts_decode_attn_events(*args, events[0].h, events[1].h), "ts_decode_attn_events")
     return workspace
+
+
+def decode_attn_noalloc(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale: float,
+                        max_ctx_len: Optional[int] = None, num_workers: int = 0, stream=None,
+                        variant: int = 0) -> None:
+    """ts_decode_attn_noalloc on torch tensors (no workspace: the library's
+    static device scratch)."""
+    _check_tensors(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out)
+    shape = shape_of(q, k_pages, page_table, max_ctx_len, num_workers, variant)
+    check(lib.ts_decode_attn_noalloc(ctypes.byref(shape), q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
+                                     page_table.data_ptr(), ctx_lens.data_ptr(), q_lens.data_ptr(),
+                                     out.data_ptr(), ctypes.c_float(scale), _stream_ptr(stream)),
+          "ts_decode_attn_noalloc")
 
 
 def synth_fill(t, seed: int, stream_id: int, index_offset: int = 0, stream=None) -> None:

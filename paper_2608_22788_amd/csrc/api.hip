@@ -220,7 +220,7 @@ static bool debug_enabled() {
     return v == 1;
 }
 
-static int launch(const ts_attn_shape *s, const void *q, const void *k_pages, const void *v_pages,
+int launch_attn(const ts_attn_shape *s, const void *q, const void *k_pages, const void *v_pages,
                   const int32_t *page_table, const int32_t *ctx_lens, const int32_t *q_lens,
                   void *out, float scale, void *workspace, size_t workspace_bytes, void *stream,
                   void *ev_begin, void *ev_end) {
@@ -364,7 +364,7 @@ int ts_decode_attn(const ts_attn_shape *shape, const void *q, const void *k_page
                    const int32_t *q_lens, void *out, float scale, void *workspace,
                    size_t workspace_bytes, void *stream) {
     try {
-        return launch(shape, q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale,
+        return launch_attn(shape, q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale,
                       workspace, workspace_bytes, stream, nullptr, nullptr);
     } catch (...) {
         return fail(TS_ERR_HIP, "unexpected C++ exception");
@@ -377,7 +377,7 @@ int ts_decode_attn_events(const ts_attn_shape *shape, const void *q, const void 
                           float scale, void *workspace, size_t workspace_bytes, void *stream,
                           void *ev_begin, void *ev_end) {
     try {
-        return launch(shape, q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale,
+        return launch_attn(shape, q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale,
                       workspace, workspace_bytes, stream, ev_begin, ev_end);
     } catch (...) {
         return fail(TS_ERR_HIP, "unexpected C++ exception");
