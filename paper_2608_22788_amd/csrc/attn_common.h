@@ -64,6 +64,29 @@ __device__ __forceinline__ u32x2_t ld_stream8(const void *p) {
     return __builtin_nontemporal_load(reinterpret_cast<const u32x2_t *>(p));
 }
 
+// A (page, KV head) block as a buffer resource.  Loads at byte offsets below
+// `bytes` read the block; a load at or past `bytes` returns zeros without a
+// memory access, so bytes = 0 turns the loads of a page past the segment end
+// into no-ops that yield zeros (no branch, no clamped re-read).  Word 3 is the
+// raw 32-bit data format of the gfx9 family's buffer descriptors.
+typedef __amdgpu_buffer_rsrc_t block_rsrc_t;
+constexpr int kBufferWord3 = 0x00020000;
+constexpr int kLoadNt = 2;   // cache policy of buffer loads: non-temporal
+
+__device__ __forceinline__ block_rsrc_t block_rsrc(const void *base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes, kBufferWord3);
+}
+__device__ __forceinline__ u32x4_t ld_block16(block_rsrc_t r, int byte_off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kLoadNt);
+}
+__device__ __forceinline__ u32x2_t ld_block8(block_rsrc_t r, int byte_off) {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, byte_off, 0, kLoadNt);
+}
+
+// Keeps the instruction scheduler from moving anything across this point, so
+// the program order of a prefetch relative to the computation is kept.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));

@@ -25,7 +25,10 @@
 //   * the running reference m_ref of each row is only raised when a score
 //     exceeds it by more than 8 in log2 units, which leaves the accumulators
 //     untouched on almost every page;
-//   * pages are prefetched kRing - 1 ahead into a ring of registers.
+//   * the next page is loaded into a second register set while the current
+//     one is computed; loads go through a buffer resource bounded to the
+//     page's block, so a prefetch past the segment end reads nothing (it used
+//     to re-read the last page: about 0.8 % of the bulk call's traffic).
 // Masks: key t is visible to draft row i iff t <= L - Q + i; keys past the
 // segment end or the context end get probability 0 and their value rows are
 // zeroed before the product, so stale data never reaches the output.
@@ -48,8 +51,8 @@ struct VRow;
 template <>
 struct VRow<8> {
     uint32_t w[4];
-    __device__ void load(const uint16_t *p) {
-        const u32x4_t t = ld_stream16(p);
+    __device__ void load(block_rsrc_t r, int byte_off) {
+        const u32x4_t t = ld_block16(r, byte_off);
         w[0] = t.x; w[1] = t.y; w[2] = t.z; w[3] = t.w;
     }
     __device__ void zero() { w[0] = w[1] = w[2] = w[3] = 0; }
@@ -57,8 +60,8 @@ struct VRow<8> {
 template <>
 struct VRow<4> {
     uint32_t w[2];
-    __device__ void load(const uint16_t *p) {
-        const u32x2_t t = ld_stream8(p);
+    __device__ void load(block_rsrc_t r, int byte_off) {
+        const u32x2_t t = ld_block8(r, byte_off);
         w[0] = t.x; w[1] = t.y;
     }
     __device__ void zero() { w[0] = w[1] = 0; }
@@ -68,25 +71,28 @@ template <int D, int NB>
 struct Verify {
     static constexpr int KS = D / 32;   // k-steps of the score product
     static constexpr int VE = D / 16;   // value dims per lane = P.V products per row block
-    static constexpr int kRing = 2;   // pages in the register ring
+    static constexpr int kBlockBytes = kPage * D * 2;   // one (page, KV head) block
 
     struct PageRegs {
         u32x4_t k[KS];      // A operands of the score product
         VRow<VE> v[4];      // value rows of the lane's 4 tokens
     };
 
-    __device__ static void load_page(const AttnParams &p, const int32_t *pt, int j, int g, int n,
+    // Page j of the segment [.., j1); past the segment the loads are no-ops
+    // that yield zeros (the page is then computed fully masked).
+    __device__ static void load_page(const AttnParams &p, const int32_t *pt, int j, int j1, int g, int n,
                                      int kq, PageRegs &r) {
-        const int pid = ld_meta(pt, j);
+        const bool in = j < j1;
+        const int pid = ld_meta(pt, in ? j : j1 - 1);
         const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * D);
-        const uint16_t *kb = p.k_pages + base + (size_t)n * D + 8 * kq;
+        const block_rsrc_t rk = block_rsrc(p.k_pages + base, in ? kBlockBytes : 0);
+        const block_rsrc_t rv = block_rsrc(p.v_pages + base, in ? kBlockBytes : 0);
 #pragma unroll
         for (int s = 0; s < KS; s++)
-            r.k[s] = ld_stream16(kb + 32 * s);
-        const uint16_t *vb = p.v_pages + base + (size_t)(4 * kq) * D + VE * n;
+            r.k[s] = ld_block16(rk, 2 * (n * D + 8 * kq + 32 * s));
 #pragma unroll
         for (int i = 0; i < 4; i++)
-            r.v[i].load(vb + (size_t)i * D);
+            r.v[i].load(rv, 2 * ((4 * kq + i) * D + VE * n));
     }
 
     // Element e (0..VE-1) of a VE-wide bf16 row held in dwords.
@@ -201,18 +207,17 @@ struct Verify {
         // keys below this bound are visible to every row of the block
         const int full_end = min(L - Q + 1, seg_end_tok);
 
-        // Prefetches are issued unconditionally with the page index clamped to
-        // the segment: a load under a branch would make the compiler wait for
-        // it before the current page is computed.
+        // Prefetches are issued unconditionally: a page past the segment is
+        // loaded through a buffer resource with no records (zeros, no memory
+        // access), so no load sits under a branch.
+        constexpr int kRing = 2;
         PageRegs ring[kRing];
-#pragma unroll
-        for (int k = 0; k < kRing - 1; k++)
-            load_page(p, pt, min(s.j0 + k, s.j1 - 1), g, n, kq, ring[k]);
+        load_page(p, pt, s.j0, s.j1, g, n, kq, ring[0]);
         for (int j = s.j0; j < s.j1; j += kRing) {
 #pragma unroll
             for (int k = 0; k < kRing; k++) {
                 if (j + k < s.j1) {
-                    load_page(p, pt, min(j + k + kRing - 1, s.j1 - 1), g, n, kq, ring[(k + kRing - 1) % kRing]);
+                    load_page(p, pt, j + k + kRing - 1, s.j1, g, n, kq, ring[(k + kRing - 1) % kRing]);
                     page_step(p, st, ring[k], j + k, full_end, seg_end_tok, kq);
                 }
             }

@@ -12,8 +12,10 @@
 // A workgroup is one worker of the stream-K partition (attn_common.h).
 //
 // Staging.  A page is loaded as eight 1 KiB slabs, one 16-byte piece per
-// lane: four K slabs (slab s holds, for consumer lane l = 16 kq + n, key row
-// n dims 32 s + 8 kq .. + 7: the A operand of the score product, stored in
+// lane, through a buffer resource bounded to the page's block (so a group
+// past the segment end reads nothing): four K slabs (slab s holds, for
+// consumer lane l = 16 kq + n, key row n dims 32 s + 8 kq .. + 7: the A
+// operand of the score product, stored in
 // lane order so reads are conflict-free consecutive 16 bytes) and four V
 // slabs (slab i: value row 4 kq + i, dims 8 n .. 8 n + 7), stored as the
 // page's 16 value rows in natural order with a 288-byte row pitch.  The four
@@ -79,6 +81,7 @@ constexpr int kVPitch = 288;              // bytes per value row in LDS
 constexpr int kVOff = 4 * kSlab;          // value rows follow the K slabs
 constexpr int kPageLds = kVOff + kPage * kVPitch;   // one staged page
 constexpr int kTeam = 4;                  // wavefronts per workgroup
+constexpr int kBlockBytes = kPage * kD * 2;   // one (page, KV head) block
 
 template <int NBE>
 struct Team {
@@ -110,23 +113,25 @@ struct Team {
         }
     };
 
-    // Issue this wave's loads of group `grp` (pages j0 + grp * GP + q).  Pages
-    // past the segment are clamped to its last page rather than skipped: a load
-    // under a branch would make the compiler wait for it at the join.
+    // Issue this wave's loads of group `grp` (pages j0 + grp * GP + q): K slab
+    // `wave` and V slab `wave` of each page, i.e. slots tau = wave + 4 t with
+    // t = 2 q (K) and t = 2 q + 1 (V).  Loads go through a buffer resource
+    // bounded to the page's block; for a page past the segment it has no
+    // records, so the loads read nothing and yield zeros (no branch, no
+    // re-read of the last page).
     __device__ __forceinline__ static void load_group(const AttnParams &p, const int32_t *pt, int g, int j0, int j1,
                                       int grp, int wave, int lane, Regs &r) {
         const int n = lane & 15, kq = lane >> 4;
 #pragma unroll
-        for (int t = 0; t < PER_WAVE; t++) {
-            const int tau = wave + kTeam * t;
-            const int po = tau >> 3, sl = tau & 7;
-            const int j = min(j0 + grp * GP + po, j1 - 1);
-            const int pid = ld_meta(pt, j);
+        for (int q = 0; q < GP; q++) {
+            const int j = j0 + grp * GP + q;
+            const bool in = j < j1;
+            const int pid = ld_meta(pt, in ? j : j1 - 1);
             const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * kD);
-            const size_t off = sl < 4 ? (size_t)n * kD + 32 * sl + 8 * kq
-                                      : (size_t)(4 * kq + sl - 4) * kD + 8 * n;
-            const uint16_t *src = (sl < 4 ? p.k_pages : p.v_pages) + base + off;
-            r.s[t] = ld_stream16(src);
+            const block_rsrc_t rk = block_rsrc(p.k_pages + base, in ? kBlockBytes : 0);
+            const block_rsrc_t rv = block_rsrc(p.v_pages + base, in ? kBlockBytes : 0);
+            r.s[2 * q] = ld_block16(rk, 2 * (n * kD + 32 * wave + 8 * kq));
+            r.s[2 * q + 1] = ld_block16(rv, 2 * ((4 * kq + wave) * kD + 8 * n));
         }
     }
 

@@ -49,18 +49,57 @@ __global__ __launch_bounds__(kReadThreads) void read_kernel(const u32x4_t *src, 
 
 // Reads, for every page an attention call with the same arguments streams,
 // the whole K block and V block of each KV head, in the attention kernels'
-// worker partition (attn_common.h) and with their non-temporal 16-byte loads,
-// kGatherBatch pages in flight per wavefront.  Nothing is computed beyond
-// folding the words into one per lane (written to `sink`), so its bandwidth
-// is the ceiling of the paged access pattern itself: random 32 D-byte blocks
-// found through the page table.
-constexpr int kGatherBatch = 4;
+// worker partition (attn_common.h) and with their loads: the same lanes read
+// the same 16-byte pieces through a buffer resource bounded to the block, one
+// page in flight while the previous one is consumed, and a prefetch past the
+// segment end reads nothing.  Nothing is computed beyond folding the words
+// into one per lane (written to `sink`), so its bandwidth is the ceiling of
+// the paged access pattern itself: random 32 D-byte blocks found through the
+// page table.
+template <int D>
+struct GatherPage {
+    static constexpr int KS = D / 32;          // 16-byte K pieces per lane
+    static constexpr int VE = D / 16;          // value dims per lane
+    static constexpr int kBlockBytes = kPage * D * 2;
+    u32x4_t k[KS];
+    u32x4_t v[4];      // at D = 64 only .x, .y are loaded (8 bytes per row)
+
+    __device__ __forceinline__ void load(const AttnParams &p, const int32_t *pt, int j, int j1, int g, int lane) {
+        const int n = lane & 15, kq = lane >> 4;
+        const bool in = j < j1;
+        const int pid = ld_meta(pt, in ? j : j1 - 1);
+        const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * D);
+        const block_rsrc_t rk = block_rsrc(p.k_pages + base, in ? kBlockBytes : 0);
+        const block_rsrc_t rv = block_rsrc(p.v_pages + base, in ? kBlockBytes : 0);
+#pragma unroll
+        for (int s = 0; s < KS; s++)
+            k[s] = ld_block16(rk, 2 * (n * D + 8 * kq + 32 * s));
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            if constexpr (VE == 8) {
+                v[i] = ld_block16(rv, 2 * ((4 * kq + i) * D + VE * n));
+            } else {
+                const u32x2_t t = ld_block8(rv, 2 * ((4 * kq + i) * D + VE * n));
+                v[i] = u32x4_t{t.x, t.y, 0u, 0u};
+            }
+        }
+    }
+    __device__ __forceinline__ uint32_t fold() const {
+        uint32_t a = 0;
+#pragma unroll
+        for (int s = 0; s < KS; s++)
+            a ^= k[s].x ^ k[s].y ^ k[s].z ^ k[s].w;
+#pragma unroll
+        for (int i = 0; i < 4; i++)
+            a ^= v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
+        return a;
+    }
+};
 
 template <int D>
 __global__ __launch_bounds__(kWave) void page_gather_kernel(AttnParams p, uint32_t *sink) {
     extern __shared__ int s_pre[];
     page_prefix(p, s_pre);
-    constexpr int kLoads = kPage * D * 2 / (16 * kWave);   // 16-byte loads per lane per block
     const int lane = threadIdx.x;
     const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
     const int w = blockIdx.x;
@@ -69,27 +108,18 @@ __global__ __launch_bounds__(kWave) void page_gather_kernel(AttnParams p, uint32
     for (int64_t x = worker_begin(ptot, w, p.W); x < end;) {
         const Segment s = locate(p, s_pre, x, end);
         const int32_t *pt = p.page_table + (size_t)s.b * p.max_pages;
-        for (int j = s.j0; j < s.j1; j += kGatherBatch) {
-            u32x4_t v[kGatherBatch][2 * kLoads];
-#pragma unroll
-            for (int u = 0; u < kGatherBatch; u++) {
-                // clamped to the segment's last page (not folded twice): a
-                // load under a branch would be waited for at the join
-                const int pid = ld_meta(pt, j + u < s.j1 ? j + u : s.j1 - 1);
-                const size_t base = ((size_t)pid * p.Hkv + s.g) * (size_t)(kPage * D) + 8 * lane;
-#pragma unroll
-                for (int i = 0; i < kLoads; i++) {
-                    v[u][i] = ld_stream16(p.k_pages + base + 8 * kWave * i);
-                    v[u][kLoads + i] = ld_stream16(p.v_pages + base + 8 * kWave * i);
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < kGatherBatch; u++)
-                if (j + u < s.j1) {
-#pragma unroll
-                    for (int i = 0; i < 2 * kLoads; i++)
-                        acc ^= fold(v[u][i]);
-                }
+        GatherPage<D> r0, r1;
+        r0.load(p, pt, s.j0, s.j1, s.g, lane);
+        sched_fence();
+        for (int j = s.j0; j < s.j1; j += 2) {
+            r1.load(p, pt, j + 1, s.j1, s.g, lane);
+            sched_fence();
+            acc ^= r0.fold();
+            sched_fence();
+            r0.load(p, pt, j + 2, s.j1, s.g, lane);
+            sched_fence();
+            acc ^= r1.fold();   // zeros for a page past the segment
+            sched_fence();
         }
         x = s.next;
     }
