@@ -303,7 +303,9 @@ int launch_attn(const ts_attn_shape *s, const void *q, const void *k_pages, cons
     // The single-wavefront kernels combine their splits themselves when there
     // are at least twice as many units as workers (a unit then has one or two
     // pieces); otherwise the merge kernel does.
-    p.fuse_splits = !pl.team && (int64_t)p.B * p.Hkv >= 2 * (int64_t)p.W;
+    const size_t o_bytes = pl.ws_lse_off - pl.ws_o_off;
+    p.fuse_splits = !pl.team && (int64_t)p.B * p.Hkv >= 2 * (int64_t)p.W && o_bytes < ((size_t)1 << 31);
+    p.ws_o_bytes = p.fuse_splits ? (int)o_bytes : 0;
 
     hipError_t e;
     if (p.fuse_splits) {

@@ -48,6 +48,7 @@ struct AttnParams {
     int rows_per_unit;          // G * Qmax
     int W;                      // workers (wavefronts)
     int fuse_splits;            // single-wavefront kernels: combine splits in the kernel
+    int ws_o_bytes;             // bytes of the partial area (set when fuse_splits; < 2^31)
     float scale_log2;           // scale * log2(e)
 };
 

@@ -285,8 +285,8 @@ struct DecodeQ1 {
                                                 o[r][8 * c + 2] * inv, o[r][8 * c + 3] * inv};
                             const f32x4_t hi = {o[r][8 * c + 4] * inv, o[r][8 * c + 5] * inv,
                                                 o[r][8 * c + 6] * inv, o[r][8 * c + 7] * inv};
-                            st_coherent16(dst + 64 * c + 8 * part, lo);
-                            st_coherent16(dst + 64 * c + 8 * part + 4, hi);
+                            st_partial16(p, row * D + 64 * c + 8 * part, lo);
+                            st_partial16(p, row * D + 64 * c + 8 * part + 4, hi);
                         }
                         if (part == 0)
                             st_coherent(p.ws_lse + row, lse);

@@ -21,21 +21,33 @@ namespace tsattn {
 constexpr int kMergeBatch = 8;
 
 // Loads and stores coherent across the whole device (the L2 caches of all
-// XCDs): relaxed atomics at agent scope, which on gfx950 are plain global
-// loads and stores with the device-scope cache policy.  A store is visible
-// device-wide once the issuing wavefront's vector memory counter has drained.
+// XCDs), so that the worker combining a unit sees the partials the others
+// wrote in the same launch.  Scalar ones are relaxed atomics at agent scope;
+// the 16-byte ones are buffer loads and stores over the partial area with the
+// device-scope cache policy (the host combines in the kernel only while that
+// area is below 2 GiB, so byte offsets fit the buffer's 32-bit offsets).  On
+// gfx950 both are plain memory operations with that policy bit, and a store
+// is visible device-wide once the issuing wavefront's vector memory counter
+// has drained.
+constexpr int kDeviceScope = 16;   // cache policy of buffer operations: sc1
+
 __device__ __forceinline__ float ld_coherent(const float *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void st_coherent(float *p, float v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// 16 bytes (p 16-byte aligned) as two 8-byte device-scope stores.
-__device__ __forceinline__ void st_coherent16(float *p, f32x4_t v) {
-    uint64_t *q = reinterpret_cast<uint64_t *>(p);
-    const f32x2_t lo = {v[0], v[1]}, hi = {v[2], v[3]};
-    __hip_atomic_store(q, __builtin_bit_cast(uint64_t, lo), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(q + 1, __builtin_bit_cast(uint64_t, hi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ block_rsrc_t partial_rsrc(const AttnParams &p) {
+    return block_rsrc(p.ws_o, p.ws_o_bytes);
+}
+// Partial-area elements elem .. elem + 3 (elem a multiple of 4).
+__device__ __forceinline__ void st_partial16(const AttnParams &p, size_t elem, f32x4_t v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), partial_rsrc(p),
+                                           (int)(elem * sizeof(float)), 0, kDeviceScope);
+}
+__device__ __forceinline__ f32x4_t ld_partial16(const AttnParams &p, size_t elem) {
+    return __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                           partial_rsrc(p), (int)(elem * sizeof(float)), 0, kDeviceScope));
 }
 // Waits until every vector memory operation this wavefront issued is
 // complete.  The wait itself is not a memory operation to the compiler, so
@@ -109,9 +121,10 @@ struct Acc {
             if constexpr (kCoherent) {
                 l[k] = k < n ? ld_coherent(p.ws_lse + row) : -INFINITY;
 #pragma unroll
-                for (int e = 0; e < VE / 4; e++)
-                    v[k][e] = make_float4(ld_coherent(src + 4 * e), ld_coherent(src + 4 * e + 1),
-                                          ld_coherent(src + 4 * e + 2), ld_coherent(src + 4 * e + 3));
+                for (int e = 0; e < VE / 4; e++) {
+                    const f32x4_t t = ld_partial16(p, row * D + VE * part + 4 * e);
+                    v[k][e] = make_float4(t[0], t[1], t[2], t[3]);
+                }
             } else {
                 l[k] = k < n ? p.ws_lse[row] : -INFINITY;
 #pragma unroll

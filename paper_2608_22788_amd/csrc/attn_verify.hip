@@ -253,8 +253,9 @@ struct Verify {
                         // device-coherent: the unit's last arriver combines it
 #pragma unroll
                         for (int e = 0; e < VE; e += 4)
-                            st_coherent16(dst + e, f32x4_t{st.acc[rb][e][i] * inv, st.acc[rb][e + 1][i] * inv,
-                                                           st.acc[rb][e + 2][i] * inv, st.acc[rb][e + 3][i] * inv});
+                            st_partial16(p, row * D + VE * n + e,
+                                         f32x4_t{st.acc[rb][e][i] * inv, st.acc[rb][e + 1][i] * inv,
+                                                 st.acc[rb][e + 2][i] * inv, st.acc[rb][e + 3][i] * inv});
                         if (n == 0)
                             st_coherent(p.ws_lse + row, lse);
                     } else {
