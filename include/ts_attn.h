@@ -35,20 +35,23 @@
  * library allocates nothing inside ts_decode_attn, never synchronises it and
  * never reads device data on the host, so a call can be captured into a HIP
  * graph.  Inputs are read-only; out is written only at rows i < q_lens[b]
- * (q_lens[b] = 0 skips sequence b).  The workspace holds split partial
- * results, the arrival counters of the in-kernel combine (cleared by the call
- * itself) and the TS_DEBUG flag word; it needs no initialisation, its contents
- * are undefined on return, and a workspace can be reused by any later call,
- * of any shape, on one stream.  Calls that may run concurrently need distinct
- * workspaces.  Every entry point
+ * (q_lens[b] = 0 skips sequence b).  The workspace starts with a fixed
+ * 1 MiB area of arrival counters (one per (sequence, KV head)), then the
+ * TS_DEBUG flag word, then split partial results.  It must be zero-filled
+ * before its first use (e.g. hipMemset once after allocation); every completed
+ * call leaves the counters zero again and never writes anything else over
+ * them, so a workspace can be reused by any later call, of any shape, on one
+ * stream (the rest of its contents is undefined on return).  Calls that may
+ * run concurrently need distinct workspaces.  Every entry point
  * returns TS_OK (0) or a negative ts_status; on error nothing is launched and
  * ts_last_error() describes the cause.  No C++ exception crosses the ABI.
  *
  * Device-side preconditions (1 <= q_lens[b] <= ctx_lens[b] <= max_ctx_len,
  * ctx_lens[b] <= max_pages_per_seq * page_size, q_lens[b] <= max_q_len, page
  * ids in [0, num_pages)) are the caller's to keep on the fast path; with the
- * environment variable TS_DEBUG=1 a checking kernel verifies them first, the
- * call synchronises and returns TS_ERR_SHAPE if any fails.
+ * environment variable TS_DEBUG=1 a checking kernel verifies them (and that
+ * the workspace counters are zero) first, the call synchronises and returns
+ * TS_ERR_SHAPE (TS_ERR_WORKSPACE for the counters) if any fails.
  */
 #ifndef TS_ATTN_H
 #define TS_ATTN_H
@@ -119,8 +122,8 @@ size_t ts_decode_attn_workspace_size(const ts_attn_shape *shape);
 /* Paged decode / verify attention as defined above, enqueued on `stream`
  * (a hipStream_t; NULL is the default stream).  `scale` multiplies the dot
  * products (typically 1/sqrt(head_dim)).  `workspace` is device memory of at
- * least ts_decode_attn_workspace_size(shape) bytes, 256-byte aligned, with
- * any contents. */
+ * least ts_decode_attn_workspace_size(shape) bytes, 256-byte aligned,
+ * zero-filled before its first use (see above). */
 int ts_decode_attn(const ts_attn_shape *shape, const void *q, const void *k_pages,
                    const void *v_pages, const int32_t *page_table, const int32_t *ctx_lens,
                    const int32_t *q_lens, void *out, float scale, void *workspace,
@@ -146,8 +149,9 @@ int ts_decode_attn_events(const ts_attn_shape *shape, const void *q, const void 
  * the array are rejected with TS_ERR_WORKSPACE before anything is launched
  * (every shape with num_workers = 0 fits).  Every call on one GPU shares that
  * GPU's array, so calls that may overlap on one GPU (different streams, or
- * graphs replayed concurrently) race and must not be issued; the call clears
- * what it needs zeroed itself. */
+ * graphs replayed concurrently) race and must not be issued.  The array starts
+ * zeroed and every call leaves its arrival counters zero, as with a
+ * zero-filled workspace. */
 #define TS_NOALLOC_SCRATCH_BYTES ((size_t)48 << 20)
 
 int ts_decode_attn_noalloc(const ts_attn_shape *shape, const void *q, const void *k_pages,

@@ -193,11 +193,10 @@ def _check_tensors(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out):
 
 
 def new_workspace(nbytes: int, device="cuda"):
-    """A workspace of nbytes.  The library needs no particular contents, so
-    it is filled with a non-zero byte pattern: every caller then exercises
-    that contract."""
+    """A zero-filled workspace of nbytes (the library requires zeros before
+    the first use and leaves its split counters zero after every call)."""
     import torch
-    return torch.full((nbytes,), 0xA7, dtype=torch.uint8, device=device)
+    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
 
 
 def decode_attn(q, k_pages, v_pages, page_table, ctx_lens, q_lens, out, scale: float,

@@ -24,9 +24,8 @@ kernel_fn decode_q1_variant(int D, int G);
 kernel_fn verify_variant(int D, int NB);
 kernel_fn verify_team_variant(int rows, int *lds_bytes, int *nbe);
 kernel_fn merge_variant(int D, bool few);
-void (*clear_counters_fn())(int *, int);
 int debug_check(const ts_attn_shape *s, const int32_t *page_table, const int32_t *ctx_lens,
-                const int32_t *q_lens, int *flags, hipStream_t stream);
+                const int32_t *q_lens, const int *counters, int *flags, hipStream_t stream);
 
 static thread_local std::string g_last_error;
 
@@ -198,8 +197,9 @@ int make_plan(const ts_attn_shape *s, Plan *pl) {
                (s->variant == TS_VARIANT_TEAM || (s->variant == TS_VARIANT_AUTO && pl->NB >= 3));
     pl->auto_w = s->num_workers == 0;
     pl->W = s->num_workers > 0 ? s->num_workers : auto_workers(s, pl->q1, pl->team, pl->rows_per_unit);
-    // Workspace: the split counters first (one per unit, cleared by each call
-    // that uses them), then 256 bytes for the TS_DEBUG check's flag word, then
+    // Workspace: the split counters first, at a fixed size whatever the shape,
+    // so that no call's partial results ever land on them (they are zero
+    // between calls); then 256 bytes for the TS_DEBUG check's flag word; then
     // the partial outputs and their log-sum-exp.
     const size_t slots = 2 * (size_t)pl->W;
     pl->ws_cnt_off = 0;
@@ -248,7 +248,7 @@ int launch_attn(const ts_attn_shape *s, const void *q, const void *k_pages, cons
     int *counters = reinterpret_cast<int *>(static_cast<char *>(workspace) + pl.ws_cnt_off);
     if (debug_enabled()) {
         int *flags = reinterpret_cast<int *>(static_cast<char *>(workspace) + pl.ws_dbg_off);
-        st = debug_check(s, page_table, ctx_lens, q_lens, flags, hs);
+        st = debug_check(s, page_table, ctx_lens, q_lens, counters, flags, hs);
         if (st)
             return st;
     }
@@ -308,13 +308,6 @@ int launch_attn(const ts_attn_shape *s, const void *q, const void *k_pages, cons
     p.ws_o_bytes = p.fuse_splits ? (int)o_bytes : 0;
 
     hipError_t e;
-    if (p.fuse_splits) {
-        // the arrival counters of this call's units start at zero
-        const int n = p.B * p.Hkv;
-        hipLaunchKernelGGL(clear_counters_fn(), dim3((n + 255) / 256), dim3(256), 0, hs, counters, n);
-        if ((e = hipGetLastError()) != hipSuccess)
-            return hip_fail(e, "counter clear launch");
-    }
     if (ev_begin || ev_end) {
         // the events take the kernel's own start and end timestamps
         void *args[] = {&p};

@@ -114,20 +114,9 @@ __global__ __launch_bounds__(kWaves * 64) void merge_few_kernel(AttnParams p) {
         write_merged<D>(p, b, g, r, part, a);
 }
 
-// Sets the call's n arrival counters to zero before the streaming kernel
-// counts on them (a plain fill kernel, so the call needs no memset node and
-// the workspace needs no preparation).
-__global__ __launch_bounds__(256) void clear_counters_kernel(int *counters, int n) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n)
-        counters[i] = 0;
-}
-
 }  // namespace
 
 typedef void (*kernel_fn)(AttnParams);
-
-void (*clear_counters_fn())(int *, int) { return clear_counters_kernel; }
 
 kernel_fn merge_variant(int D, bool few) {
     if (D == 64)

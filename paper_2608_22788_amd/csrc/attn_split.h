@@ -200,7 +200,8 @@ __device__ __forceinline__ void write_merged(const AttnParams &p, int b, int g, 
 
 // Combines all pieces of unit (b, g) and writes its rows (one wavefront;
 // rows_per_unit rows, 4 per pass; rows of draft positions >= q_len are
-// skipped).  Called by the worker that counted the last arrival on the unit.
+// skipped).  Called by the worker that counted the last arrival on the unit,
+// which then sets the counter back to zero for the next call.
 template <int D>
 __device__ void combine_unit(const AttnParams &p, int b, int g, const UnitSplit &u, int lane) {
     const int part = lane & 15;
@@ -215,14 +216,17 @@ __device__ void combine_unit(const AttnParams &p, int b, int g, const UnitSplit 
         if (row_ok)
             write_merged<D>(p, b, g, r, part, a);
     }
+    // every arrival has been counted: leave the counter zero for the next call
+    __hip_atomic_store(p.counters + (size_t)b * p.Hkv + g, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Counts this wavefront's arrival on the unit of a piece whose partial it has
 // just written with device-coherent stores; the last arriver combines the
 // unit.  The stores are complete once the vector memory counter has drained,
 // so no cache-wide fence is needed, and the last arriver's loads are issued
-// after its count returned.  The counters start at zero: the call clears
-// them before the streaming kernel runs.
+// after its count returned.  The counters are zero between calls (the
+// workspace is zero-filled before its first use, and the last arriver of each
+// unit resets its counter).
 template <int D>
 __device__ void arrive_and_combine(const AttnParams &p, const Segment &s, int64_t ptot, int lane) {
     wait_vmem();

@@ -7,8 +7,11 @@
 // ends.  In host code `scratch` names a host-side stand-in, not a device
 // address, so its address on each device is looked up once, with that device
 // current, and only that address is handed to kernels.  Every call on one GPU
-// shares that GPU's array: calls that overlap on one GPU race; the call clears
-// the counters it relies on before its kernels count on them.
+// shares that GPU's array, so calls that overlap on one GPU race.  The array
+// has static storage and starts zeroed; the arrival counters of the in-kernel
+// combine (its first 1 MiB) are the only part that must start at zero, and
+// every call leaves them zero again (the last arriver of each unit resets its
+// counter), exactly as a zero-filled caller workspace.
 #include <hip/hip_runtime.h>
 
 #include <mutex>

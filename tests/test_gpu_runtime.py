@@ -1,7 +1,8 @@
 """Runtime contracts of the C ABI on the GPU: a call can be captured into a
 HIP graph and replayed, TS_DEBUG=1 turns violated device-side preconditions
-into TS_ERR_SHAPE before any attention kernel runs (with its flag word in the
-call's own workspace), and calls on two streams with their own workspaces do
+into TS_ERR_SHAPE (a workspace whose counters are not zero into
+TS_ERR_WORKSPACE) before any attention kernel runs, with its flag word in the
+call's own workspace, and calls on two streams with their own workspaces do
 not interfere."""
 import os
 import subprocess
@@ -76,17 +77,19 @@ DEBUG_SCRIPT = textwrap.dedent("""
         device.run(wl, t3); results.append("no error")
     except binding.TsError as e:
         results.append(str(e.status) + ":" + str(e))
-    # a workspace of arbitrary bytes passes the check, gives the result of a
-    # fresh one, and the failed checks above left no flag behind in it
-    fresh = torch.zeros((8 << 20,), dtype=torch.uint8, device="cuda")
-    device.run(wl, t, num_workers=7, workspace=fresh)
+    # a reused workspace passes the check after every call (its counters are
+    # left zero, and the failed checks above left no flag that matters); one
+    # that was never zero-filled is reported
+    ws = binding.new_workspace(8 << 20)
+    for _ in range(3):
+        device.run(wl, t, num_workers=7, workspace=ws)
     torch.cuda.synchronize()
-    ref = t["out"].clone()
-    dirty = torch.full((8 << 20,), 0xFF, dtype=torch.uint8, device="cuda")
-    for _ in range(2):
-        device.run(wl, t, num_workers=7, workspace=dirty)
-    torch.cuda.synchronize()
-    results.append("same" if torch.equal(t["out"].view(torch.int16), ref.view(torch.int16)) else "differs")
+    results.append("reuse ok")
+    dirty = torch.full((8 << 20,), 1, dtype=torch.uint8, device="cuda")
+    try:
+        device.run(wl, t, workspace=dirty); results.append("no error")
+    except binding.TsError as e:
+        results.append(str(e.status) + ":" + str(e))
     print("RESULTS", results)
 """)
 
@@ -100,7 +103,8 @@ def test_debug_mode_reports_bad_device_inputs():
     line = [ln for ln in r.stdout.splitlines() if ln.startswith("RESULTS")][0]
     assert "-2:" in line.split("'")[1] and "page id" in line
     assert line.count("-2:") == 2 and "q_lens" in line
-    assert line.endswith("'same']")
+    assert "'reuse ok'" in line
+    assert line.count("-3:") == 1 and "zero-fill" in line
 
 
 def test_concurrent_streams_with_their_own_workspaces():
