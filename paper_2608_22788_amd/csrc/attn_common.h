@@ -203,6 +203,17 @@ __device__ inline void page_prefix(const AttnParams &p, int *s_pre) {
     __syncthreads();
 }
 
+// Worker of workgroup `block` (of W): the chip deals workgroups to its 8 XCDs
+// round-robin (workgroup b runs on XCD b % 8), and each XCD has its own L2.
+// Consecutive workers of the partition share units (a unit's pieces, its
+// query rows and page-table entries), so they are given consecutive
+// workgroups of one XCD: XCD x takes workers base(x) .. base(x + 1) - 1.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_worker(int block, int W) {
+    const int x = block % kXcds, s = block / kXcds;
+    return x * (W / kXcds) + min(x, W % kXcds) + s;
+}
+
 __device__ __forceinline__ int64_t worker_begin(int64_t ptot, int w, int W) {
     return (ptot * (int64_t)w) / (int64_t)W;
 }

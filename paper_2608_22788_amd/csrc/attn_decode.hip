@@ -316,7 +316,7 @@ __global__ __launch_bounds__(64) void decode_q1_kernel(AttnParams p) {
     extern __shared__ int s_pre[];
     page_prefix(p, s_pre);
     const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
-    const int w = blockIdx.x;
+    const int w = xcd_worker(blockIdx.x, p.W);
     const int64_t begin = worker_begin(ptot, w, p.W);
     const int64_t end = worker_begin(ptot, w + 1, p.W);
     for (int64_t x = begin; x < end;) {

@@ -416,7 +416,7 @@ __global__ __launch_bounds__(256) void verify_team_kernel(AttnParams p) {
     page_prefix(p, s_pre);
     char *lds = reinterpret_cast<char *>(s_pre) + (((p.B + 1) * 4 + 15) & ~15);
     const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
-    const int w = blockIdx.x;
+    const int w = xcd_worker(blockIdx.x, p.W);
     const int64_t begin = worker_begin(ptot, w, p.W);
     const int64_t end = worker_begin(ptot, w + 1, p.W);
     for (int64_t x = begin; x < end;) {

@@ -102,7 +102,7 @@ __global__ __launch_bounds__(kWave) void page_gather_kernel(AttnParams p, uint32
     page_prefix(p, s_pre);
     const int lane = threadIdx.x;
     const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
-    const int w = blockIdx.x;
+    const int w = xcd_worker(blockIdx.x, p.W);
     const int64_t end = worker_begin(ptot, w + 1, p.W);
     uint32_t acc = 0;
     for (int64_t x = worker_begin(ptot, w, p.W); x < end;) {
