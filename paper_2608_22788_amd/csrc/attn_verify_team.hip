@@ -11,14 +11,16 @@
 // each.
 // A workgroup is one worker of the stream-K partition (attn_common.h).
 //
-// Staging.  A page is loaded as eight 1 KiB slabs, one 16-byte piece per
+// Staging.  A page is loaded as eight 1 KiB pieces, one 16-byte piece per
 // lane, through a buffer resource bounded to the page's block (so a group
-// past the segment end reads nothing): four K slabs (slab s holds, for
-// consumer lane l = 16 kq + n, key row n dims 32 s + 8 kq .. + 7: the A
-// operand of the score product, stored in
-// lane order so reads are conflict-free consecutive 16 bytes) and four V
-// slabs (slab i: value row 4 kq + i, dims 8 n .. 8 n + 7), stored as the
-// page's 16 value rows in natural order with a 288-byte row pitch.  The four
+// past the segment end reads nothing).  Wave w loads K rows 4 w .. 4 w + 3
+// whole (1 KiB contiguous, so each 128-byte line is fetched by one load) and
+// scatters them into four K slabs (slab s holds, for consumer lane
+// l = 16 kq + n, key row n dims 32 s + 8 kq .. + 7: the A operand of the
+// score product, stored in lane order with the 16-byte chunk index swizzled
+// so that the scattered writes and the reads are free of bank conflicts) and
+// four V slabs (slab i: value row 4 kq + i, dims 8 n .. 8 n + 7), stored as
+// the page's 16 value rows in natural order with a 288-byte row pitch.  The four
 // waves split the loading; loads run kDepth groups ahead in registers, are
 // written into one of two LDS stages, and one barrier per page group
 // separates writing a stage from reading it.
@@ -130,20 +132,31 @@ struct Team {
             const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * kD);
             const block_rsrc_t rk = block_rsrc(p.k_pages + base, in ? kBlockBytes : 0);
             const block_rsrc_t rv = block_rsrc(p.v_pages + base, in ? kBlockBytes : 0);
-            r.s[2 * q] = ld_block16(rk, 2 * (n * kD + 32 * wave + 8 * kq));
+            // K rows 4 wave .. 4 wave + 3 whole (1 KiB contiguous per load):
+            // lane l holds row 4 wave + l / 16, dims 8 (l % 16) .. + 7
+            r.s[2 * q] = ld_block16(rk, 2 * ((4 * wave + kq) * kD + 8 * n));
             r.s[2 * q + 1] = ld_block16(rv, 2 * ((4 * kq + wave) * kD + 8 * n));
         }
     }
 
+    // Where 16-byte chunk C of a page's K slabs is stored (C = 64 slab +
+    // consumer lane): its low four bits are XORed with the next four, so that
+    // both the scattered writes below and the consumers' reads touch sixteen
+    // distinct bank groups per sixteen lanes.
+    __device__ __forceinline__ static int k_chunk(int C) { return C ^ ((C >> 4) & 15); }
+
+    // Writes the wave's loads of a group into a stage.  A K piece (row rho =
+    // 4 wave + kq, 8-dim chunk c = n) goes where the score product's A operand
+    // wants it: slab c / 4, consumer lane 16 (c % 4) + rho (swizzled).  A V
+    // piece (row 4 kq + wave, dims 8 n .. + 7) goes to its row in natural order.
     __device__ __forceinline__ static void store_group(char *stage, int wave, int lane, const Regs &r) {
         const int n = lane & 15, kq = lane >> 4;
+        const int k_off = k_chunk(64 * (n >> 2) + 16 * (n & 3) + 4 * wave + kq) * 16;
+        const int v_off = kVOff + (4 * kq + wave) * kVPitch + 16 * n;
 #pragma unroll
         for (int t = 0; t < PER_WAVE; t++) {
-            const int tau = wave + kTeam * t;
-            const int po = tau >> 3, sl = tau & 7;
-            char *pg = stage + po * kPageLds;
-            char *dst = sl < 4 ? pg + sl * kSlab + lane * 16 : pg + kVOff + (4 * kq + sl - 4) * kVPitch + 16 * n;
-            *reinterpret_cast<u32x4_t *>(dst) = r.s[t];
+            char *pg = stage + (t >> 1) * kPageLds;
+            *reinterpret_cast<u32x4_t *>(pg + ((t & 1) ? v_off : k_off)) = r.s[t];
         }
     }
 
@@ -164,7 +177,7 @@ struct Team {
         u32x4_t kf[4];
 #pragma unroll
         for (int s = 0; s < 4; s++)
-            kf[s] = ld16(pg + s * kSlab + lane * 16);
+            kf[s] = ld16(pg + k_chunk(64 * s + lane) * 16);
         // transpose-read address of this lane for product jj: + 32 jj bytes
         typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
         const char *vbase = pg + kVOff + (4 * kq + (n >> 2)) * kVPitch + 8 * (n & 3);
