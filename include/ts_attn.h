@@ -36,7 +36,8 @@
  * never reads device data on the host, so a call can be captured into a HIP
  * graph.  Inputs are read-only; out is written only at rows i < q_lens[b]
  * (q_lens[b] = 0 skips sequence b).  The workspace starts with a fixed
- * 1 MiB area of arrival counters (one per (sequence, KV head)), then the
+ * 1 MiB area of arrival counters (one per (sequence, KV head), up to 4 KiB
+ * apart when there are few), then the
  * TS_DEBUG flag word, then split partial results.  It must be zero-filled
  * before its first use (e.g. hipMemset once after allocation); every completed
  * call leaves the counters zero again and never writes anything else over
@@ -131,8 +132,10 @@ int ts_decode_attn(const ts_attn_shape *shape, const void *q, const void *k_page
 
 /* ts_decode_attn whose main (KV-streaming) kernel is launched with `ev_begin`
  * and `ev_end` attached to its dispatch: they take the kernel's own start and
- * end timestamps, so ts_event_elapsed_ms() gives that kernel's duration alone.
- * Events come from ts_event_create(); either may be NULL. */
+ * end timestamps, so ts_event_elapsed_ms() gives that kernel's duration alone
+ * (with the combination of split results when that launch does it, without
+ * the separate merge kernel when one follows).  Events come from
+ * ts_event_create(); either may be NULL. */
 int ts_decode_attn_events(const ts_attn_shape *shape, const void *q, const void *k_pages,
                           const void *v_pages, const int32_t *page_table,
                           const int32_t *ctx_lens, const int32_t *q_lens, void *out,
@@ -194,7 +197,7 @@ typedef struct ts_sweep_point {
     int32_t num_pools;          /* distinct KV pools rotated through */
     int64_t sum_ctx;            /* sum of context lengths */
     int64_t kv_bytes;           /* algorithmic K+V bytes per call */
-    double t_median_us;         /* per-call time, whole call (main + merge) */
+    double t_median_us;         /* per-call time, whole call (every launch it makes) */
     double t_p10_us;
     double t_p90_us;
     double kv_gbps;             /* kv_bytes / t_median */

@@ -300,38 +300,75 @@ int launch_attn(const ts_attn_shape *s, const void *q, const void *k_pages, cons
             pl.W = resident;
         p.W = pl.W;
     }
-    // The single-wavefront kernels combine their splits themselves when there
-    // are at least twice as many units as workers (a unit then has one or two
-    // pieces); otherwise the merge kernel does.
+    // Who combines the splits (attn_split.h):
+    //  * the last worker of a unit, for the single-wavefront kernels with at
+    //    least twice as many units as workers (a unit has one or two pieces);
+    //  * merge wavefronts appended to the grid, one per row of each unit, when
+    //    units have many pieces (a unit meets about W / units + 1 workers;
+    //    here W >= 8 units) and that takes at most kMaxMergeWgs workgroups;
+    //  * otherwise the merge kernel after the launch, and always when the
+    //    partial area is too large for 32-bit buffer offsets.
+    // Measured against the merge kernel (median call; 32/8 heads, head_dim
+    // 128): in the launch it is 3-9 % faster for 1-4 sequences with q_len 4,
+    // 2-7 % for 1-16 sequences with q_len 1 and 1 % on the block-draft
+    // workload (4 sequences, 64 rows).  With 1,024 merge wavefronts (8
+    // sequences with q_len 4, the MTP workload) it was 1-2 % slower, and so
+    // was it with 2-4 pieces per unit (64-128 sequences), hence the bounds.
+    constexpr int64_t kMaxMergeWgs = 512;
     const size_t o_bytes = pl.ws_lse_off - pl.ws_o_off;
-    p.fuse_splits = !pl.team && (int64_t)p.B * p.Hkv >= 2 * (int64_t)p.W && o_bytes < ((size_t)1 << 31);
-    p.ws_o_bytes = p.fuse_splits ? (int)o_bytes : 0;
+    const int64_t units = (int64_t)p.B * p.Hkv;
+    const int ngroups = (pl.rows_per_unit + 3) / 4;
+    const int64_t merge_wgs = units * (pl.team ? ngroups : pl.rows_per_unit);
+    p.combine = kCombineKernel;
+    if (o_bytes < ((size_t)1 << 31)) {
+        if (!pl.team && units >= 2 * (int64_t)p.W)
+            p.combine = kCombineLast;
+        else if ((int64_t)p.W >= 8 * units && merge_wgs <= kMaxMergeWgs)
+            p.combine = kCombineInLaunch;
+    }
+    p.ws_o_bytes = p.combine != kCombineKernel ? (int)o_bytes : 0;
+    // Counters of consecutive units up to 4 KiB apart (inside the counter
+    // area) when merge wavefronts poll them.
+    p.cnt_shift = 0;
+    if (p.combine == kCombineInLaunch)
+        while (p.cnt_shift < 10 && units << (p.cnt_shift + 1) <= kMaxUnits)
+            p.cnt_shift++;
+    const unsigned grid = (unsigned)(p.W + (p.combine == kCombineInLaunch ? merge_wgs : 0));
+    if (p.combine == kCombineInLaunch && pl.team && pl.auto_w) {
+        // Reserve enough LDS that only the workers' teams fit on a compute
+        // unit (their registers would allow one more): a merge workgroup then
+        // starts where a team has finished instead of polling beside two
+        // streaming teams from the start, which measured 1 % faster.
+        const size_t lds_cu = (size_t)160 * 1024;
+        const int teams = per_cu_bound(false, true, pl.rows_per_unit);
+        const size_t gate = ((lds_cu / teams + lds_cu / (teams + 1)) / 2) & ~(size_t)1023;
+        if (main_lds < gate)
+            main_lds = gate;
+    }
 
     hipError_t e;
     if (ev_begin || ev_end) {
         // the events take the kernel's own start and end timestamps
         void *args[] = {&p};
-        e = hipExtLaunchKernel(reinterpret_cast<const void *>(main_k), dim3(pl.W), dim3(main_threads), args,
+        e = hipExtLaunchKernel(reinterpret_cast<const void *>(main_k), dim3(grid), dim3(main_threads), args,
                                main_lds, hs, reinterpret_cast<hipEvent_t>(ev_begin),
                                reinterpret_cast<hipEvent_t>(ev_end), 0);
         if (e != hipSuccess)
             return hip_fail(e, "attention kernel launch");
     } else {
-        hipLaunchKernelGGL(main_k, dim3(pl.W), dim3(main_threads), main_lds, hs, p);
+        hipLaunchKernelGGL(main_k, dim3(grid), dim3(main_threads), main_lds, hs, p);
     }
     if ((e = hipGetLastError()) != hipSuccess)
         return hip_fail(e, "attention kernel launch");
-    if (p.fuse_splits)
-        return TS_OK;   // the kernel combined its own splits
+    if (p.combine != kCombineKernel)
+        return TS_OK;   // the launch combined its own splits
     // A unit meets about W / units + 1 workers.  Up to about three pieces a
     // unit, one wavefront per 4 rows takes every piece itself (a fourth of
     // the blocks); beyond that four wavefronts share each row group's pieces.
     // Measured: 1,024 units with 16-32 rows, 768-1,024 workers, 1.5-6 %
     // faster per call; at 4 pieces a unit (32 skewed sequences) the long
     // sequences' units made it 2 % slower, hence the bound.
-    const int64_t units = (int64_t)p.B * p.Hkv;
     const bool few = (int64_t)p.W <= 2 * units;
-    const int ngroups = (pl.rows_per_unit + 3) / 4;
     const int64_t merge_blocks = units * (few ? (ngroups + 3) / 4 : ngroups);
     hipLaunchKernelGGL(few ? merge_variant(p.D, true) : merge_k, dim3((unsigned)merge_blocks), dim3(4 * kWave), lds,
                        hs, p);

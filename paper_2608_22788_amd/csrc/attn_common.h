@@ -13,9 +13,10 @@
 // and log2-sum-exp go to the workspace, slot 2w if the piece is the first of
 // the worker's range and 2w+1 otherwise.  A unit processed whole by one worker
 // is written straight to `out`.  The workers that touched a unit are found by
-// inverting the range formula, and their slots are combined (attn_split.h):
-// by the last of them to finish (one-token decode kernel, many units) or by a
-// separate merge kernel.
+// inverting the range formula, and their slots are combined (attn_split.h) in
+// one of three ways, chosen on the host: by the last of them to finish (many
+// units, one or two pieces each), by merge workgroups appended to the same
+// launch (few units, many pieces each), or by a separate merge kernel.
 // Everything depends on ctx_lens / q_lens read on the device, so the launch
 // grid depends on the shape alone.
 #pragma once
@@ -32,7 +33,14 @@ constexpr int kMaxUnits = 1 << 18; // (sequence, KV head) units per call
 constexpr size_t kCounterBytes = (size_t)kMaxUnits * sizeof(int);   // split counters
 constexpr float kRescaleSlack = 8.0f;  // lazy rescale threshold, log2 units
 
-struct AttnParams {
+// Who combines the split partials of a launch.  In the two in-launch modes
+// the workers write partials with device-coherent stores and count their
+// arrivals on the unit's counter.
+constexpr int kCombineKernel = 0;    // a separate merge kernel (plain stores)
+constexpr int kCombineLast = 1;      // the last worker to finish a piece of the unit
+constexpr int kCombineInLaunch = 2;  // merge workgroups after the W workers of the grid
+
+struct AttnParams {   // 128 bytes of kernel arguments
     const uint16_t *q;          // [B][Qmax][Hq][D] bf16
     const uint16_t *k_pages;    // [num_pages][Hkv][P][D] bf16
     const uint16_t *v_pages;
@@ -42,13 +50,14 @@ struct AttnParams {
     uint16_t *out;              // [B][Qmax][Hq][D] bf16
     float *ws_o;                // [2W][rows_per_unit][D] fp32 partial outputs
     float *ws_lse;              // [2W][rows_per_unit] fp32 log2-sum-exp
-    int *counters;              // [B][Hkv] arrivals per split unit (zero between calls)
+    int *counters;              // arrivals per split unit, unit u at u << cnt_shift (zero between calls)
     int B, Hq, Hkv, D, Qmax, max_pages;
     int G;                      // Hq / Hkv
     int rows_per_unit;          // G * Qmax
     int W;                      // workers (wavefronts)
-    int fuse_splits;            // single-wavefront kernels: combine splits in the kernel
-    int ws_o_bytes;             // bytes of the partial area (set when fuse_splits; < 2^31)
+    int ws_o_bytes;             // bytes of the partial area (set unless kCombineKernel; < 2^31)
+    int16_t combine;            // kCombine*: who combines the split partials
+    int16_t cnt_shift;          // log2 of the ints between the counters of consecutive units
     float scale_log2;           // scale * log2(e)
 };
 
@@ -133,6 +142,11 @@ __device__ __forceinline__ float sum8(float x) {
 }
 
 __device__ __forceinline__ int first_lane_int(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Split counter of unit (b, g).
+__device__ __forceinline__ int *unit_counter(const AttnParams &p, int unit) {
+    return p.counters + ((size_t)unit << p.cnt_shift);
+}
 
 // Metadata (page table, context and draft lengths) is read-only for the whole
 // launch.  Reading it through the constant address space lets wavefront-uniform

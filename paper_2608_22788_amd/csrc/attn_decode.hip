@@ -25,17 +25,20 @@
 //     pair; the row sum is accumulated from the same rounded probabilities;
 //   * at the end of a segment the 8 slots are merged with log-sum-exp
 //     weights through cross-lane shuffles.
-// With p.fuse_splits set, splits are combined in this kernel: a wavefront
-// that wrote a partial (a piece of a unit that other workers share) with
-// device-coherent stores waits for them to complete, then counts its arrival
-// on the unit's counter; the one that arrives last combines all partials of
-// the unit (device-coherent loads), writes the output rows and sets the
-// counter back to zero.  No cache-wide write-back or invalidation is needed.
-// This saves the merge kernel's launch but puts four dependent memory round
-// trips (store, count, partial loads, output) at the end of the last pieces;
-// the host enables it when units are at least twice as many as workers (a
-// unit then has one or two pieces), where it was measured faster (4-5 % at
-// 256 sequences), and otherwise launches the merge kernel.
+// Unless p.combine is kCombineKernel, splits are combined in this launch: a
+// wavefront that wrote a partial (a piece of a unit that other workers share)
+// with device-coherent stores waits for them to complete, then counts its
+// arrival on the unit's counter.  With kCombineLast it counts right after the
+// piece, and the one that arrives last combines all partials of the unit
+// (device-coherent loads), writes the output rows and sets the counter back
+// to zero; with kCombineInLaunch it counts after its whole range, and the
+// merge wavefronts that follow the workers in the grid combine (attn_split.h).
+// No cache-wide write-back or invalidation is needed.  kCombineLast saves
+// the merge kernel's launch but puts four dependent memory round trips
+// (store, count, partial loads, output) at the end of the last pieces; the
+// host takes it when units are at least twice as many as workers (a unit
+// then has one or two pieces), where it was measured faster (4-5 % at 256
+// sequences).
 // Masking: only the last page of a sequence has slots past the context end;
 // their probabilities are forced to 0 and their value rows to 0, so stale
 // data (even NaN) in unused slots never reaches the output.
@@ -276,9 +279,9 @@ struct DecodeQ1 {
                     const size_t row = (size_t)slot_id * p.rows_per_unit + r;
                     float *dst = p.ws_o + row * D;
                     const float lse = l > 0.0f ? M + __log2f(l) : -INFINITY;
-                    if (p.fuse_splits) {
-                        // device-coherent stores: another worker of this
-                        // launch may combine them (arrive_and_combine)
+                    if (p.combine != kCombineKernel) {
+                        // device-coherent stores: another wavefront of this
+                        // launch combines them
 #pragma unroll
                         for (int c = 0; c < NC; c++) {
                             const f32x4_t lo = {o[r][8 * c + 0] * inv, o[r][8 * c + 1] * inv,
@@ -306,7 +309,7 @@ struct DecodeQ1 {
                 }
             }
         }
-        if (!s.whole && p.fuse_splits)
+        if (!s.whole && p.combine == kCombineLast)
             arrive_and_combine<D>(p, s, ptot, lane);
     }
 };
@@ -315,15 +318,24 @@ template <int D, int G>
 __global__ __launch_bounds__(64) void decode_q1_kernel(AttnParams p) {
     extern __shared__ int s_pre[];
     page_prefix(p, s_pre);
+    if (__builtin_expect((int)blockIdx.x >= p.W, 0)) {   // merge workgroups, laid out after the workers' code
+        const int m = (int)blockIdx.x - p.W;
+        merge_in_launch<D>(p, s_pre, m / p.rows_per_unit, m % p.rows_per_unit);
+        return;
+    }
     const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
     const int w = xcd_worker(blockIdx.x, p.W);
     const int64_t begin = worker_begin(ptot, w, p.W);
     const int64_t end = worker_begin(ptot, w + 1, p.W);
+    Arrivals arr;
+    arr.init();
     for (int64_t x = begin; x < end;) {
         const Segment s = locate(p, s_pre, x, end);
         DecodeQ1<D, G>::segment(p, s, x == begin ? 2 * w : 2 * w + 1, ptot);
+        arr.add(p, s);
         x = s.next;
     }
+    arr.flush<false>(p);
 }
 
 }  // namespace

@@ -1,6 +1,7 @@
 // attn_merge.hip -- combines the split partial results of units that more
-// than one worker processed, whenever the streaming kernel did not combine
-// them itself.  The combination rule and the lane layout are in attn_split.h.
+// than one worker processed, whenever the streaming launch did not combine
+// them itself (kCombineKernel).  The combination rule and the lane layout
+// are in attn_split.h.
 //
 // Two shapes of the same work, chosen on the host from the expected number
 // of pieces per unit:
@@ -52,31 +53,10 @@ __global__ __launch_bounds__(kWaves * 64) void merge_kernel(AttnParams p) {
     gather_partials<D, false>(p, u, rr, part, wave, kWaves, a);   // wave w takes partials w, w + 4, ...
 
     // combine the waves' running sums (lane-wise) through LDS
-    __shared__ float s_comb[kWaves - 1][VE + 2][64];
-    if (wave > 0) {
-#pragma unroll
-        for (int e = 0; e < VE; e++)
-            s_comb[wave - 1][e][lane] = a.acc[e];
-        s_comb[wave - 1][VE][lane] = a.den;
-        s_comb[wave - 1][VE + 1][lane] = a.M;
-    }
-    __syncthreads();
+    __shared__ float s_comb[(kWaves - 1) * (VE + 2) * 64];
+    combine_waves<VE, kWaves>(a, s_comb, wave, lane);
     if (wave != 0 || !row_ok)
         return;
-    float Mall = a.M;
-#pragma unroll
-    for (int w = 0; w < kWaves - 1; w++)
-        Mall = fmaxf(Mall, s_comb[w][VE + 1][lane]);
-    a.rescale(Mall);
-#pragma unroll
-    for (int w = 0; w < kWaves - 1; w++) {
-        const float Mw = s_comb[w][VE + 1][lane];
-        const float f = Mw == -INFINITY ? 0.0f : fast_exp2(Mw - Mall);
-        a.den += f * s_comb[w][VE][lane];
-#pragma unroll
-        for (int e = 0; e < VE; e++)
-            a.acc[e] += f * s_comb[w][e][lane];
-    }
     write_merged<D>(p, b, g, r, part, a);
 }
 

@@ -45,6 +45,11 @@ __device__ __forceinline__ void st_partial16(const AttnParams &p, size_t elem, f
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), partial_rsrc(p),
                                            (int)(elem * sizeof(float)), 0, kDeviceScope);
 }
+// Partial-area element elem.
+__device__ __forceinline__ void st_partial4(const AttnParams &p, size_t elem, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), partial_rsrc(p), (int)(elem * sizeof(float)), 0,
+                                          kDeviceScope);
+}
 __device__ __forceinline__ f32x4_t ld_partial16(const AttnParams &p, size_t elem) {
     return __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
                                            partial_rsrc(p), (int)(elem * sizeof(float)), 0, kDeviceScope));
@@ -217,26 +222,197 @@ __device__ void combine_unit(const AttnParams &p, int b, int g, const UnitSplit 
             write_merged<D>(p, b, g, r, part, a);
     }
     // every arrival has been counted: leave the counter zero for the next call
-    __hip_atomic_store(p.counters + (size_t)b * p.Hkv + g, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(unit_counter(p, b * p.Hkv + g), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Counts this wavefront's arrival on the unit of a piece whose partial it has
-// just written with device-coherent stores; the last arriver combines the
-// unit.  The stores are complete once the vector memory counter has drained,
-// so no cache-wide fence is needed, and the last arriver's loads are issued
-// after its count returned.  The counters are zero between calls (the
-// workspace is zero-filled before its first use, and the last arriver of each
-// unit resets its counter).
+// kCombineLast: counts this wavefront's arrival on the unit of a piece whose
+// partial it has just written with device-coherent stores; the last arriver
+// combines the unit.  The stores are complete once the vector memory counter
+// has drained, so no cache-wide fence is needed, and the last arriver's loads
+// are issued after its count returned.  The counters are zero between calls
+// (the workspace is zero-filled before its first use, and each call leaves
+// them zero).
 template <int D>
 __device__ void arrive_and_combine(const AttnParams &p, const Segment &s, int64_t ptot, int lane) {
     wait_vmem();
     int old = 0;
     if (lane == 0)
-        old = atomicAdd(p.counters + (size_t)s.b * p.Hkv + s.g, 1);
+        old = atomicAdd(unit_counter(p, s.b * p.Hkv + s.g), 1);
     old = first_lane_int(old);
     const UnitSplit u = unit_split(ptot, s.us, s.np, p.W);
     if (old == u.nparts - 1)
         combine_unit<D>(p, s.b, s.g, u, lane);
+}
+
+// kCombineInLaunch: a worker has split pieces in at most two units (the first
+// and the last segment of its range) and counts its arrivals on them once,
+// after its whole range: every piece of a split unit ends near the end of
+// the launch anyway, and a drain of the stores between segments would stall
+// the worker for a memory round trip.
+struct Arrivals {
+    int u0, u1;   // units of the pending arrivals, -1 for none
+    __device__ __forceinline__ void init() { u0 = u1 = -1; }
+    __device__ __forceinline__ void add(const AttnParams &p, const Segment &s) {
+        if (!s.whole && p.combine == kCombineInLaunch) {
+            const int u = s.b * p.Hkv + s.g;
+            if (u0 < 0)
+                u0 = u;
+            else
+                u1 = u;
+        }
+    }
+    // Called by every thread of the workgroup; the first thread counts.
+    template <bool kBlock>
+    __device__ __forceinline__ void flush(const AttnParams &p) {
+        if (u0 < 0)
+            return;
+        wait_vmem();
+        if constexpr (kBlock)
+            __syncthreads();   // every wavefront's stores are complete
+        if (threadIdx.x == 0) {
+            atomicAdd(unit_counter(p, u0), 1);
+            if (u1 >= 0)
+                atomicAdd(unit_counter(p, u1), 1);
+        }
+    }
+};
+
+// Sums of waves 1 .. kWaves - 1 of a workgroup added into wave 0's `a` (the
+// same lanes of each wave hold the same rows and dims), through LDS at
+// `comb` (3 * (VE + 2) * 64 floats).  Every thread of the workgroup calls it.
+template <int VE, int kWaves>
+__device__ void combine_waves(Acc<VE> &a, float *comb, int wave, int lane) {
+    float(*c)[VE + 2][64] = reinterpret_cast<float(*)[VE + 2][64]>(comb);
+    if (wave > 0) {
+#pragma unroll
+        for (int e = 0; e < VE; e++)
+            c[wave - 1][e][lane] = a.acc[e];
+        c[wave - 1][VE][lane] = a.den;
+        c[wave - 1][VE + 1][lane] = a.M;
+    }
+    __syncthreads();
+    if (wave != 0)
+        return;
+    float Mall = a.M;
+#pragma unroll
+    for (int w = 0; w < kWaves - 1; w++)
+        Mall = fmaxf(Mall, c[w][VE + 1][lane]);
+    if (Mall == -INFINITY)
+        return;   // no partial saw a visible key: the sums stay zero
+    a.rescale(Mall);
+#pragma unroll
+    for (int w = 0; w < kWaves - 1; w++) {
+        const float Mw = c[w][VE + 1][lane];
+        const float f = Mw == -INFINITY ? 0.0f : fast_exp2(Mw - Mall);
+        a.den += f * c[w][VE][lane];
+#pragma unroll
+        for (int e = 0; e < VE; e++)
+            a.acc[e] += f * c[w][e][lane];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Merge wavefronts in the streaming launch (kCombineInLaunch).
+//
+// The grid holds the W workers and then the merge workgroups, one wavefront
+// per row of each unit (single-wavefront kernels: workgroup W + m is row
+// m % R of unit m / R; four-wavefront kernels: wave w of workgroup W + m is
+// row 4 (m % ceil(R / 4)) + w of unit m / ceil(R / 4)).  A merge wavefront
+// waits until every worker with a piece of its unit has counted its arrival,
+// then its four 16-lane groups read pieces k, k + 4, ... (k = lane / 16)
+// with device-coherent loads, so up to 4 * kMergeBatch pieces cost one
+// memory round trip; the groups' sums meet through cross-lane exchanges and
+// group 0 writes the row.  The host takes this mode for units with many
+// pieces (a few long sequences), where the merge kernel's launch after the
+// whole grid was a large share of a short call.
+//
+// Forward progress: the dispatcher starts the workgroups of each XCD in
+// increasing order, so every worker has started before any merge workgroup
+// of its XCD, and workers never wait.  A merge wavefront therefore only
+// waits for workgroups that are running.  The wait is bounded all the same
+// (kMergeSpins polls); a wavefront that gives up writes NaN, so such a
+// failure shows in the output instead of as a hang.
+//
+// Counter protocol: the unit's counter reaches nparts once every worker has
+// arrived; then each merge wavefront of the unit with a valid row adds one
+// after it has read the partials, and the last of them sets the counter back
+// to zero for the next call.  The host spaces the counters of the units
+// apart (cnt_shift): with all of them on one line, every worker's arrival
+// and every merge wavefront's poll queued on that line, which made the
+// block-draft call 38 % slower.
+constexpr int kMergeSpins = 1 << 22;
+
+// Waits until *c >= target; false if kMergeSpins polls saw less.
+__device__ __forceinline__ bool wait_count(const int *c, int target) {
+    for (int i = 0; i < kMergeSpins; i++) {
+        const int v = first_lane_int(__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        if (v >= target) {
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);   // later loads stay after the poll
+            return true;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    return false;
+}
+
+// Sums of the four 16-lane groups (same part, different pieces) combined;
+// every group gets the total.
+template <int VE>
+__device__ __forceinline__ void combine_lane_groups(Acc<VE> &a) {
+    float Mall = fmaxf(a.M, __shfl_xor(a.M, 16));
+    Mall = fmaxf(Mall, __shfl_xor(Mall, 32));
+    const float f = a.M == -INFINITY ? 0.0f : fast_exp2(a.M - Mall);
+    float den = a.den * f;
+    den += __shfl_xor(den, 16);
+    den += __shfl_xor(den, 32);
+    a.den = den;
+#pragma unroll
+    for (int e = 0; e < VE; e++) {
+        float v = a.acc[e] * f;
+        v += __shfl_xor(v, 16);
+        v += __shfl_xor(v, 32);
+        a.acc[e] = v;
+    }
+    a.M = Mall;
+}
+
+// Combines and writes row r of unit `unit` (one wavefront).
+template <int D>
+__device__ void merge_in_launch(const AttnParams &p, const int *s_pre, int unit, int r) {
+    const int b = unit / p.Hkv, g = unit % p.Hkv;
+    const int np = s_pre[b + 1] - s_pre[b];
+    if (np == 0)
+        return;
+    const int nvalid = min(p.rows_per_unit, ld_meta(p.q_lens, b) * p.G);   // rows with i < q_len
+    if (r >= nvalid)
+        return;
+    const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
+    const int64_t us = (int64_t)p.Hkv * s_pre[b] + (int64_t)g * np;
+    const UnitSplit u = unit_split(ptot, us, np, p.W);
+    if (u.wlo == u.whi)
+        return;   // one worker saw the whole unit and wrote `out`
+    const int lane = threadIdx.x & 63;
+    int *cnt = unit_counter(p, unit);
+    const bool ok = wait_count(cnt, u.nparts);
+    Acc<D / 16> a;
+    a.init();
+    if (ok) {
+        gather_partials<D, true>(p, u, r, lane & 15, lane >> 4, 4, a);
+    } else {
+#pragma unroll
+        for (int e = 0; e < D / 16; e++)
+            a.acc[e] = __builtin_nanf("");
+        a.den = 1.0f;
+        a.M = 0.0f;
+    }
+    combine_lane_groups(a);
+    if (lane < 16)
+        write_merged<D>(p, b, g, r, lane, a);
+    if (lane == 0) {
+        const int old = atomicAdd(cnt, 1);
+        if (old == u.nparts + nvalid - 1)   // nvalid merge wavefronts per unit
+            __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
 }  // namespace tsattn

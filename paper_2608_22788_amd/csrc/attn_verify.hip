@@ -32,8 +32,9 @@
 // Masks: key t is visible to draft row i iff t <= L - Q + i; keys past the
 // segment end or the context end get probability 0 and their value rows are
 // zeroed before the product, so stale data never reaches the output.
-// With p.fuse_splits the last worker to finish a piece of a unit combines the
-// unit's pieces itself (attn_split.h) instead of the merge kernel.
+// Splits are combined as p.combine says (attn_split.h): by the last worker to
+// finish a piece of the unit, by the merge wavefronts that follow the workers
+// in the grid (workgroups W and up), or by the separate merge kernel.
 #include "attn_split.h"
 
 namespace tsattn {
@@ -249,8 +250,8 @@ struct Verify {
                     const size_t row = (size_t)slot_id * R + r;
                     float *dst = p.ws_o + row * D + VE * n;
                     const float lse = l > 0.0f ? m + __log2f(l) : -INFINITY;
-                    if (p.fuse_splits) {
-                        // device-coherent: the unit's last arriver combines it
+                    if (p.combine != kCombineKernel) {
+                        // device-coherent: another wavefront of this launch combines them
 #pragma unroll
                         for (int e = 0; e < VE; e += 4)
                             st_partial16(p, row * D + VE * n + e,
@@ -270,7 +271,7 @@ struct Verify {
                 }
             }
         }
-        if (!s.whole && p.fuse_splits)
+        if (!s.whole && p.combine == kCombineLast)
             arrive_and_combine<D>(p, s, ptot, lane);
     }
 };
@@ -279,15 +280,24 @@ template <int D, int NB>
 __global__ __launch_bounds__(64) void verify_kernel(AttnParams p) {
     extern __shared__ int s_pre[];
     page_prefix(p, s_pre);
+    if (__builtin_expect((int)blockIdx.x >= p.W, 0)) {   // merge workgroups, laid out after the workers' code
+        const int m = (int)blockIdx.x - p.W;
+        merge_in_launch<D>(p, s_pre, m / p.rows_per_unit, m % p.rows_per_unit);
+        return;
+    }
     const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
     const int w = xcd_worker(blockIdx.x, p.W);
     const int64_t begin = worker_begin(ptot, w, p.W);
     const int64_t end = worker_begin(ptot, w + 1, p.W);
+    Arrivals arr;
+    arr.init();
     for (int64_t x = begin; x < end;) {
         const Segment s = locate(p, s_pre, x, end);
         Verify<D, NB>::segment(p, s, x == begin ? 2 * w : 2 * w + 1, ptot);
+        arr.add(p, s);
         x = s.next;
     }
+    arr.flush<false>(p);
 }
 
 }  // namespace

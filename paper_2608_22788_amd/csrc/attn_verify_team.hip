@@ -9,7 +9,8 @@
 // it.  With 64 rows the four waves split the rows of two pages (two
 // independent chains per wave and barrier), with 16 rows they take a page
 // each.
-// A workgroup is one worker of the stream-K partition (attn_common.h).
+// A workgroup is one worker of the stream-K partition (attn_common.h), or,
+// from workgroup W on, a merge workgroup of the launch (attn_split.h).
 //
 // Staging.  A page is loaded as eight 1 KiB pieces, one 16-byte piece per
 // lane, through a buffer resource bounded to the page's block (so a group
@@ -45,7 +46,7 @@
 // states through LDS with log-sum-exp weights; the first one writes.
 // Masks: key t is visible to draft row i iff t <= L - Q + i; keys past the
 // segment or context end get probability 0 and zeroed value rows.
-#include "attn_common.h"
+#include "attn_split.h"
 
 #include <type_traits>
 
@@ -404,12 +405,22 @@ struct Team {
                     dst[16 * jj] = to_bf16(st.acc[jj][i] * inv);
             } else {
                 const size_t row = (size_t)slot_id * R + r;
-                float *dst = p.ws_o + row * kD + n;
+                const float lse = l > 0.0f ? M[i] + __log2f(l) : -INFINITY;
+                if (p.combine != kCombineKernel) {
+                    // device-coherent: merge workgroups of this launch read them
 #pragma unroll
-                for (int jj = 0; jj < 8; jj++)
-                    dst[16 * jj] = st.acc[jj][i] * inv;
-                if (n == 0)
-                    p.ws_lse[row] = l > 0.0f ? M[i] + __log2f(l) : -INFINITY;
+                    for (int jj = 0; jj < 8; jj++)
+                        st_partial4(p, row * kD + 16 * jj + n, st.acc[jj][i] * inv);
+                    if (n == 0)
+                        st_coherent(p.ws_lse + row, lse);
+                } else {
+                    float *dst = p.ws_o + row * kD + n;
+#pragma unroll
+                    for (int jj = 0; jj < 8; jj++)
+                        dst[16 * jj] = st.acc[jj][i] * inv;
+                    if (n == 0)
+                        p.ws_lse[row] = lse;
+                }
             }
         }
     }
@@ -428,15 +439,24 @@ __global__ __launch_bounds__(256) void verify_team_kernel(AttnParams p) {
     extern __shared__ int s_pre[];
     page_prefix(p, s_pre);
     char *lds = reinterpret_cast<char *>(s_pre) + (((p.B + 1) * 4 + 15) & ~15);
+    if (__builtin_expect((int)blockIdx.x >= p.W, 0)) {   // merge workgroups, laid out after the workers' code
+        const int m = (int)blockIdx.x - p.W, ngroups = (p.rows_per_unit + 3) / 4;
+        merge_in_launch<kD>(p, s_pre, m / ngroups, 4 * (m % ngroups) + (int)(threadIdx.x >> 6));
+        return;
+    }
     const int64_t ptot = (int64_t)p.Hkv * s_pre[p.B];
     const int w = xcd_worker(blockIdx.x, p.W);
     const int64_t begin = worker_begin(ptot, w, p.W);
     const int64_t end = worker_begin(ptot, w + 1, p.W);
+    Arrivals arr;
+    arr.init();
     for (int64_t x = begin; x < end;) {
         const Segment s = locate(p, s_pre, x, end);
         Team<NBE>::segment(p, s, x == begin ? 2 * w : 2 * w + 1, lds);
+        arr.add(p, s);
         x = s.next;
     }
+    arr.flush<true>(p);
 }
 
 }  // namespace

@@ -8,6 +8,7 @@
 // reports the first class of violation.
 #include <hip/hip_runtime.h>
 
+#include "attn_common.h"
 #include "ts_attn.h"
 #include "ts_internal.h"
 
@@ -44,8 +45,7 @@ __global__ __launch_bounds__(256) void check_kernel(ts_attn_shape s, const int32
             }
         }
     }
-    const int units = s.num_seqs * s.num_kv_heads;
-    for (int u = threadIdx.x; u < units; u += blockDim.x)
+    for (int u = threadIdx.x; u < (int)(kCounterBytes / sizeof(int)); u += blockDim.x)
         if (counters[u] != 0)
             bad |= kDirtyWs;
     if (bad)

@@ -198,6 +198,47 @@ def test_in_kernel_combine_with_many_pieces(dev, orc, Qmax):
             assert_parity(got, ref, f"manypieces v{var} w{w}")
 
 
+# Few units with many pieces each (workers >= 8 x units) and at most 512
+# merge workgroups: merge wavefronts that follow the workers in the grid
+# combine the splits.  (name, Hq, Hkv, D, q_lens, ctx_lens); with the
+# automatic worker count: 16 units for 768 workers (256 merge wavefronts),
+# 32 units for 1,024 (128), 16 units for 512 teams (256 workgroups).
+IN_LAUNCH = [
+    ("verify_q4", 32, 8, 128, [4, 3], [20000, 3001]),              # one draft shorter than max_q_len
+    ("decode_q1", 32, 8, 128, [1, 1, 1, 0], [9000, 40, 17000, 500]),  # a unit whole in one worker, a skipped sequence
+    ("team_q16", 32, 8, 128, [16, 5], [30000, 7000]),              # 64 rows: the team kernel
+    ("d64_g8", 64, 8, 64, [2, 2], [12000, 16]),
+]
+
+
+@pytest.mark.parametrize("case", IN_LAUNCH, ids=[c[0] for c in IN_LAUNCH])
+def test_merge_in_the_launch(dev, orc, case):
+    """Every variant, with the automatic worker count and with 4,096 workers
+    (more than one resident round, so merge workgroups start only after
+    several rounds of workers); every output element against the oracle, the
+    canaries untouched, and the workspace's counter area zero after each
+    call."""
+    import torch
+    from paper_2608_22788_amd import binding
+    _, device = dev
+    name, Hq, Hkv, D, ql, cl = case
+    wl = synth.make_workload(f"inlaunch_{name}", seed=31, cfg=small_cfg(Hq, Hkv, D), ctx_lens=cl, q_lens=ql,
+                             poison=True, spare_pages=1)
+    ref = oracle_out(orc, wl)
+    t = device.upload(wl, values="device")
+    ws = binding.new_workspace(640 << 20)
+    for var in variants_for(wl):
+        for w in (0, 4096):
+            say(f"in-launch merge {name} variant={var} workers={w}")
+            t["out_full"].fill_(device.CANARY)
+            device.run(wl, t, num_workers=w, variant=var, workspace=ws)
+            got = device.out_as_f64(t)
+            assert_parity(got, ref, f"inlaunch {name} v{var} w{w}")
+            canary_ok(t, wl)
+            torch.cuda.synchronize()
+            assert int(ws[:1 << 20].count_nonzero()) == 0, f"counters left set: {name} v{var} w{w}"
+
+
 def test_no_work_at_all():
     """Every sequence skipped (q_lens all 0): no pages carry work, every
     variant returns without touching the output."""
