@@ -40,7 +40,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.md")
 TRAFFIC_SOURCES = {
     "bulk": ["csrc/attn_common.h", "csrc/attn_split.h", "csrc/attn_verify.hip", "csrc/api.hip", "build.py"],
     "mtp": ["csrc/attn_common.h", "csrc/attn_split.h", "csrc/attn_verify.hip", "csrc/api.hip", "build.py"],
-    "dflash": ["csrc/attn_common.h", "csrc/attn_verify_team.hip", "csrc/api.hip", "build.py"],
+    "dflash": ["csrc/attn_common.h", "csrc/attn_split.h", "csrc/attn_verify_team.hip", "csrc/api.hip", "build.py"],
 }
 KERNELS = {"bulk": "verify_kernel<128,1>", "mtp": "verify_kernel<128,1>",
            "dflash": "verify_team_kernel<4>"}
