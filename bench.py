@@ -119,6 +119,13 @@ def make_pools(wl, n_pools):
 # --warmup calls (100 by default, about 50 ms).
 MIN_WARMUP_MS = 60.0
 
+# Kernel durations come from HIP events attached to the streaming kernel's
+# dispatch.  A dispatch that carries them measured about 4.6 us longer per
+# call back to back (bulk: 490.1 against 485.5 us per call, kernel 484.6 us
+# in both), so inside the timed region only every EVENT_EVERY-th call carries
+# events; the kernel average is taken over those calls.
+EVENT_EVERY = 10
+
 
 def stream_read_gbps(buf, calls=10):
     """Sequential read ceiling: the library's streaming read over `buf`
@@ -161,6 +168,7 @@ def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30, 
     shape = binding.shape_of(t["q"], t["k_pages"], t["page_table"], wl.max_ctx_len)
     ws = binding.new_workspace(binding.workspace_size(shape))
     ev = [(binding.Event(), binding.Event()) for _ in range(steps)]
+    sampled = range(0, steps, EVENT_EVERY)   # timed calls that carry kernel events
 
     def call(i, events=None):
         k, v = pools[i % n_pools]
@@ -179,11 +187,11 @@ def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30, 
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
-        call(warmup + i, ev[i])
+        call(warmup + i, ev[i] if i % EVENT_EVERY == 0 else None)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / steps
-    kern_ms = np.array([a.elapsed_ms(b) for a, b in ev])
+    kern_ms = np.array([ev[i][0].elapsed_ms(ev[i][1]) for i in sampled])
     alg = wl.algorithmic_bytes()
     extra = {}
     if ceiling:

@@ -169,9 +169,10 @@ int ts_decode_attn_noalloc(const ts_attn_shape *shape, const void *q, const void
  * context lengths (512 + a Pareto(x_min 1024, alpha 1.5) response capped at
  * 65536, the same SplitMix64 definitions as the test generator), a random
  * page permutation and N(0,1) bf16 values, then times ts_decode_attn with HIP
- * events while rotating over enough distinct KV pools to defeat the
- * last-level cache.  Synchronous; allocates its device memory once, at the
- * largest point's size, on the current device, and frees it on return. */
+ * events around groups of back-to-back calls while rotating over enough
+ * distinct KV pools to defeat the last-level cache.  Synchronous; allocates
+ * its device memory once, at the largest point's size, on the current
+ * device, and frees it on return. */
 typedef struct ts_sweep_config {
     int32_t num_q_heads;        /* 32 */
     int32_t num_kv_heads;       /* 8 */
@@ -182,7 +183,9 @@ typedef struct ts_sweep_config {
     int32_t verify_q_len;       /* ... (4); larger batches use q_len 1 */
     int32_t num_seeds;          /* seeds 0 .. num_seeds-1 per batch size */
     int32_t warmup;             /* untimed calls per point */
-    int32_t iters;              /* timed calls per point */
+    int32_t iters;              /* timed calls per point, back to back in groups of
+                                   min(10, iters / 5) calls (at least 1), so at least
+                                   five groups; a remainder is not timed */
     int64_t min_rotation_bytes; /* KV bytes cycled through per point (>= 1 GiB) */
     double verify_tokens_per_step; /* tokens a verify step emits per sequence (accepted
                                       drafts + 1); the sweep does not model acceptance,
@@ -197,8 +200,9 @@ typedef struct ts_sweep_point {
     int32_t num_pools;          /* distinct KV pools rotated through */
     int64_t sum_ctx;            /* sum of context lengths */
     int64_t kv_bytes;           /* algorithmic K+V bytes per call */
-    double t_median_us;         /* per-call time, whole call (every launch it makes) */
-    double t_p10_us;
+    double t_median_us;         /* per-call time, whole call (every launch it makes):
+                                   median over the timed groups of a group's mean */
+    double t_p10_us;            /* 10th and 90th percentiles of the same */
     double t_p90_us;
     double kv_gbps;             /* kv_bytes / t_median */
     double hbm_frac;            /* kv_gbps / 8000 (MI355X HBM3E peak) */
@@ -207,7 +211,7 @@ typedef struct ts_sweep_point {
     double tau_us;              /* t_median / tokens per step: attention time per emitted
                                    token of one sequence, the attention share of tau(b) */
     double gather_median_us;    /* per-call time of ts_page_gather_read over the same pools
-                                   (the read-only floor of the same call) */
+                                   (the read-only floor of the same call), timed alike */
 } ts_sweep_point;
 
 /* Runs the sweep; writes up to `cap` points (num_batches * num_seeds needed)

@@ -4,7 +4,8 @@
 //
 // For each batch size b and seed: draw the sweep's context lengths and page
 // permutation on the host, fill q/K/V on the device with the seeded
-// generator, then time ts_decode_attn with HIP events.  Calls rotate over
+// generator, then time ts_decode_attn with HIP events around groups of 10
+// back-to-back calls.  Calls rotate over
 // enough distinct KV pools (at least min_rotation_bytes in total) that the
 // 256 MB last-level cache cannot serve a pool from the previous call, so small
 // batches report HBM, not cache, bandwidth.  The same pools are then read by
@@ -30,6 +31,7 @@ int build_page_table(int32_t batch, const int32_t *ctx_lens, int32_t page_size,
 namespace {
 
 constexpr uint32_t kStreamQ = 4, kStreamK = 5, kStreamV = 6;
+constexpr int kGroup = 10;   // back-to-back calls per timed group
 
 struct DevBuf {
     void *p = nullptr;
@@ -158,13 +160,19 @@ int run_point(const ts_sweep_config &c, const Point &P, Arena &A, hipStream_t st
                                    static_cast<const int32_t *>(A.len.p), static_cast<const int32_t *>(A.ql.p),
                                    A.sink.p, (size_t)kGatherWorkers * 64 * 4, stream, nullptr, nullptr);
     };
+    // Timed calls run back to back in groups of up to kGroup, at least five
+    // groups, with an event after each group; a point's times are the
+    // groups' mean call times (median, p10, p90 over the groups), so a group
+    // that a host-side stall stretched does not move the median.  An event
+    // after every call measured 2.5-4 us more per call at 1-64 sequences
+    // (calls of 12-125 us), which is the cost of the event, not of the call.
+    const int group = std::max(1, std::min(kGroup, c.iters / 5));
+    const int groups = c.iters / group;
     Events evs;
-    evs.ev.resize((size_t)c.iters + 1);
+    evs.ev.resize((size_t)groups + 1);
     for (auto &ev : evs.ev)
         if ((e = hipEventCreate(&ev)))
             return hip_fail(e, "hipEventCreate");
-    // warmup calls, then iters calls with an event after each; per-call times
-    // are the differences of consecutive events (a 0..iters-1 median)
     auto timed = [&](auto &&fn, std::vector<double> &us) -> int {
         int rc;
         hipError_t he;
@@ -173,20 +181,21 @@ int run_point(const ts_sweep_config &c, const Point &P, Arena &A, hipStream_t st
                 return rc;
         if ((he = hipEventRecord(evs.ev[0], stream)))
             return hip_fail(he, "hipEventRecord");
-        for (int i = 0; i < c.iters; i++) {
-            if ((rc = fn(c.warmup + i)))
-                return rc;
-            if ((he = hipEventRecord(evs.ev[(size_t)i + 1], stream)))
+        for (int g = 0; g < groups; g++) {
+            for (int k = 0; k < group; k++)
+                if ((rc = fn(c.warmup + (int64_t)g * group + k)))
+                    return rc;
+            if ((he = hipEventRecord(evs.ev[(size_t)g + 1], stream)))
                 return hip_fail(he, "hipEventRecord");
         }
         if ((he = hipStreamSynchronize(stream)))
             return hip_fail(he, "hipStreamSynchronize");
-        us.assign((size_t)c.iters, 0.0);
-        for (int i = 0; i < c.iters; i++) {
+        us.assign((size_t)groups, 0.0);
+        for (int g = 0; g < groups; g++) {
             float ms = 0.f;
-            if ((he = hipEventElapsedTime(&ms, evs.ev[(size_t)i], evs.ev[(size_t)i + 1])))
+            if ((he = hipEventElapsedTime(&ms, evs.ev[(size_t)g], evs.ev[(size_t)g + 1])))
                 return hip_fail(he, "hipEventElapsedTime");
-            us[(size_t)i] = 1000.0 * ms;
+            us[(size_t)g] = 1000.0 * ms / group;
         }
         return TS_OK;
     };
