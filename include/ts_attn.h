@@ -263,7 +263,8 @@ size_t ts_spec_accept_workspace_size(int32_t num_seqs, int32_t vocab);
  *   num_accepted, next_token  [num_seqs]; uniforms in [0, 1).
  * The caller supplies the random numbers, so results are reproducible.  The
  * workspace (ts_spec_accept_workspace_size bytes, 256-byte aligned, any
- * contents) holds the exact block sums. */
+ * contents) holds the exact block sums and the per-sequence accepted counts
+ * between the call's two launches. */
 int ts_spec_accept(int32_t num_seqs, int32_t vocab, int32_t max_draft, const float *p_target,
                    const float *q_draft, const int32_t *draft_tokens, const int32_t *num_draft,
                    const float *u_accept, const float *u_sample, int32_t *num_accepted,

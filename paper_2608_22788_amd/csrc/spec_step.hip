@@ -93,6 +93,7 @@ struct AcceptParams {
     const float *u_sample;   // [B]
     int32_t *n_accepted, *next_token;
     uint64_t *bsum;          // [B][2][nblk][3] exact block sums of the sampling row
+    int32_t *walk;           // [B] drafts accepted, as the block-sum kernel found them
     int B, V, G, nblk;
 };
 
@@ -233,47 +234,63 @@ __device__ __forceinline__ int clamp_gamma(const AcceptParams &a, int b) {
 
 // Drafts accepted before the first rejection (gamma if none).  The test
 // u q <= p is exact: the product of two float32 values is exact in float64.
+// Every lane of the calling wavefront tests one draft (i = c + lane for
+// c = 0, 64, ...), so a walk costs two dependent loads per 64 drafts; the
+// first failing draft is the lowest set bit of the ballot.
 __device__ int accept_walk(const AcceptParams &a, int b) {
+    const int lane = threadIdx.x & (kWave - 1);
     const int gamma = clamp_gamma(a, b);
-    for (int i = 0; i < gamma; i++) {
-        const int d = a.draft[(size_t)b * a.G + i];
-        if (d < 0 || d >= a.V)
-            return i;
-        const float pv = a.p[((size_t)b * (a.G + 1) + i) * a.V + d];
-        const float qv = a.q[((size_t)b * a.G + i) * a.V + d];
-        const float p = pv > 0.0f ? fminf(pv, 1.0f) : 0.0f;
-        const float q = qv > 0.0f ? fminf(qv, 1.0f) : 0.0f;
-        const float u = clamp_uniform(a.u_accept[(size_t)b * a.G + i]);
-        if (!((double)u * (double)q <= (double)p))
-            return i;
+    for (int c = 0; c < gamma; c += kWave) {
+        const int i = c + lane;
+        bool bad = false;
+        if (i < gamma) {
+            const int d = a.draft[(size_t)b * a.G + i];
+            const float u = clamp_uniform(a.u_accept[(size_t)b * a.G + i]);
+            if (d < 0 || d >= a.V) {
+                bad = true;
+            } else {
+                const float pv = a.p[((size_t)b * (a.G + 1) + i) * a.V + d];
+                const float qv = a.q[((size_t)b * a.G + i) * a.V + d];
+                const float p = pv > 0.0f ? fminf(pv, 1.0f) : 0.0f;
+                const float q = qv > 0.0f ? fminf(qv, 1.0f) : 0.0f;
+                bad = !((double)u * (double)q <= (double)p);
+            }
+        }
+        const unsigned long long m = __ballot(bad);
+        if (m)
+            return c + __ffsll((long long)m) - 1;
     }
     return gamma;
 }
 
-// Exact weights of the sampling row at elements e .. e + 3 (zero past V): the
-// leftover mass max(0, p_k - q_k) at a rejection (use_p = false), else the
-// target row itself.
-__device__ __forceinline__ void row_weights(const AcceptParams &a, int b, int k, bool rejected, bool use_p,
-                                           int e, Fx w[4]) {
+// Elements e .. e + 3 (zero past V) of the target row p_k and, when
+// `load_q`, of the draft row q_k.
+__device__ __forceinline__ void load_rows(const AcceptParams &a, int b, int k, bool load_q, int e, float pe[4],
+                                          float qe[4]) {
     const float *prow = a.p + ((size_t)b * (a.G + 1) + k) * a.V;
-    const float *qrow = a.q + ((size_t)b * a.G + (rejected ? k : 0)) * a.V;
-    const bool resid = rejected && !use_p;
-    float pe[4], qe[4];
+    const float *qrow = a.q + ((size_t)b * a.G + (load_q ? k : 0)) * a.V;
     if (e + 3 < a.V && ((a.V & 3) == 0)) {
         const float4 pv = *reinterpret_cast<const float4 *>(prow + e);
         pe[0] = pv.x; pe[1] = pv.y; pe[2] = pv.z; pe[3] = pv.w;
-        if (resid) {
+        if (load_q) {
             const float4 qv = *reinterpret_cast<const float4 *>(qrow + e);
             qe[0] = qv.x; qe[1] = qv.y; qe[2] = qv.z; qe[3] = qv.w;
+        } else {
+            qe[0] = qe[1] = qe[2] = qe[3] = 0.0f;
         }
     } else {
 #pragma unroll
         for (int j = 0; j < 4; j++) {
             const bool in = e + j < a.V;
             pe[j] = in ? prow[e + j] : 0.0f;
-            qe[j] = (in && resid) ? qrow[e + j] : 0.0f;
+            qe[j] = (in && load_q) ? qrow[e + j] : 0.0f;
         }
     }
+}
+
+// Exact sampling weights from the loaded elements: the leftover mass
+// max(0, p_k - q_k) (resid), else the target row itself.
+__device__ __forceinline__ void weights_of(const float pe[4], const float qe[4], bool resid, Fx w[4]) {
 #pragma unroll
     for (int j = 0; j < 4; j++) {
         const Fx P = fx_of_prob(pe[j]);
@@ -284,6 +301,16 @@ __device__ __forceinline__ void row_weights(const AcceptParams &a, int b, int k,
             w[j] = P;
         }
     }
+}
+
+// The weights of the sampling row at elements e .. e + 3: the leftover mass
+// at a rejection (use_p = false), else the target row.
+__device__ __forceinline__ void row_weights(const AcceptParams &a, int b, int k, bool rejected, bool use_p,
+                                           int e, Fx w[4]) {
+    const bool resid = rejected && !use_p;
+    float pe[4], qe[4];
+    load_rows(a, b, k, resid, e, pe, qe);
+    weights_of(pe, qe, resid, w);
 }
 
 __device__ __forceinline__ Fx sum4(const Fx w[4]) {
@@ -297,6 +324,17 @@ __device__ __forceinline__ void store_fx(uint64_t *p, Fx x) {
 }
 __device__ __forceinline__ Fx load_fx(const uint64_t *p) { return Fx{p[0], p[1], p[2]}; }
 
+// Block sums j0 .. j0 + kPickChunk - 1 of a row (zero from `hi` on), every
+// load issued before any is used.
+constexpr int kPickChunk = 16;
+__device__ __forceinline__ void load_chunk(const uint64_t *bs, int j0, int hi, Fx v[kPickChunk]) {
+#pragma unroll
+    for (int c = 0; c < kPickChunk; c++) {
+        const int j = j0 + c;
+        v[c] = j < hi ? load_fx(bs + 3 * (size_t)j) : fx_zero();
+    }
+}
+
 // One wavefront per (sequence, block): the block's exact sum of sampling
 // weights.  The leftover-mass and plain-row sums are both written when a
 // rejection happened, so the pick kernel can fall back without another pass.
@@ -309,13 +347,17 @@ __global__ __launch_bounds__(256) void accept_blocks_kernel(AcceptParams a) {
     const int gamma = clamp_gamma(a, b);
     const int k = accept_walk(a, b);
     const bool rejected = k < gamma;
+    float pe[4], qe[4];
+    load_rows(a, b, k, rejected, blk * kBlk + 4 * lane, pe, qe);
     Fx w[4];
-    row_weights(a, b, k, rejected, false, blk * kBlk + 4 * lane, w);
+    weights_of(pe, qe, rejected, w);
     const Fx s = wave_sum(sum4(w));
     if (lane == 0)
         store_fx(a.bsum + (((size_t)b * 2 + 0) * a.nblk + blk) * 3, s);
+    if (blk == 0 && lane == 0)
+        a.walk[b] = k;   // read by the pick kernel, so it need not walk again
     if (rejected) {
-        row_weights(a, b, k, true, true, blk * kBlk + 4 * lane, w);
+        weights_of(pe, qe, false, w);   // the target row, from the same loads
         const Fx sp = wave_sum(sum4(w));
         if (lane == 0)
             store_fx(a.bsum + (((size_t)b * 2 + 1) * a.nblk + blk) * 3, sp);
@@ -330,19 +372,27 @@ __global__ __launch_bounds__(kPickThreads) void accept_pick_kernel(AcceptParams 
     const int b = blockIdx.x;
     const int lane = threadIdx.x;
     const int gamma = clamp_gamma(a, b);
-    const int k = __builtin_amdgcn_readfirstlane(accept_walk(a, b));
+    const int k = __builtin_amdgcn_readfirstlane(a.walk[b]);
     const bool rejected = k < gamma;
     const int per = (a.nblk + kWave - 1) / kWave;   // consecutive blocks per lane
     const int lo = min(lane * per, a.nblk), hi = min(lo + per, a.nblk);
+    // with at most kPickChunk blocks per lane (vocabularies up to 262,144),
+    // v keeps the lane's block sums for the owner's search below
+    const bool one_chunk = per <= kPickChunk;
 
     int pass = 0;
     Fx run, incl, Z;
+    Fx v[kPickChunk];
     const uint64_t *bs = nullptr;
     for (;; pass++) {
         bs = a.bsum + ((size_t)b * 2 + pass) * a.nblk * 3;
         run = fx_zero();
-        for (int j = lo; j < hi; j++)
-            run = fx_add(run, load_fx(bs + 3 * (size_t)j));
+        for (int j0 = lo; j0 < hi; j0 += kPickChunk) {
+            load_chunk(bs, j0, hi, v);
+#pragma unroll
+            for (int c = 0; c < kPickChunk; c++)
+                run = fx_add(run, v[c]);
+        }
         incl = wave_incl_scan(run, lane);
         Z = fx_shfl(incl, kWave - 1);
         // leftover mass zero: sample p_k itself (its sums are in pass 1)
@@ -366,13 +416,20 @@ __global__ __launch_bounds__(kPickThreads) void accept_pick_kernel(AcceptParams 
     Fx base = fx_zero();
     if (lane == owner) {
         Fx acc = fx_sub(incl, run);   // mass before this lane's run (incl >= run)
-        for (int j = lo; j < hi; j++) {
-            const Fx next = fx_add(acc, load_fx(bs + 3 * (size_t)j));
-            if (fx_gt(next, T)) {
-                blk = j;
-                break;
+        bool found = false;
+        for (int j0 = lo; j0 < hi && !found; j0 += kPickChunk) {
+            if (!one_chunk)
+                load_chunk(bs, j0, hi, v);
+#pragma unroll
+            for (int c = 0; c < kPickChunk; c++) {
+                const Fx next = fx_add(acc, v[c]);
+                if (!found && fx_gt(next, T)) {   // blocks past hi add zero
+                    blk = j0 + c;
+                    found = true;
+                }
+                if (!found)
+                    acc = next;
             }
-            acc = next;
         }
         base = acc;
     }
@@ -408,6 +465,12 @@ __global__ __launch_bounds__(kPickThreads) void accept_pick_kernel(AcceptParams 
 }
 
 }  // namespace
+
+// Workspace of the acceptance: the block sums, then (256-byte aligned) the
+// per-sequence walk results.
+static size_t walk_offset(size_t num_seqs, size_t nblk) {
+    return (num_seqs * 2 * nblk * 3 * sizeof(uint64_t) + 255) & ~(size_t)255;
+}
 
 }  // namespace tsattn
 
@@ -461,7 +524,7 @@ size_t ts_spec_accept_workspace_size(int32_t num_seqs, int32_t vocab) {
         return 0;
     }
     const size_t nblk = ((size_t)vocab + kBlk - 1) / kBlk;
-    return ((size_t)num_seqs * 2 * nblk * 3 * sizeof(uint64_t) + 255) & ~(size_t)255;
+    return walk_offset(num_seqs, nblk) + (((size_t)num_seqs * sizeof(int32_t) + 255) & ~(size_t)255);
 }
 
 int ts_spec_accept(int32_t num_seqs, int32_t vocab, int32_t max_draft, const float *p_target,
@@ -492,6 +555,8 @@ int ts_spec_accept(int32_t num_seqs, int32_t vocab, int32_t max_draft, const flo
     a.n_accepted = num_accepted;
     a.next_token = next_token;
     a.bsum = static_cast<uint64_t *>(workspace);
+    a.walk = reinterpret_cast<int32_t *>(static_cast<char *>(workspace) +
+                                         walk_offset(num_seqs, ((size_t)vocab + kBlk - 1) / kBlk));
     a.B = num_seqs;
     a.V = vocab;
     a.G = max_draft;
