@@ -314,9 +314,9 @@ int launch_attn(const ts_attn_shape *s, const void *q, const void *k_pages, cons
     //    here W >= 8 units) and that takes at most kMaxMergeWgs workgroups;
     //  * otherwise the merge kernel after the launch, and always when the
     //    partial area is too large for 32-bit buffer offsets.
-    // Measured against the merge kernel (median call; 32/8 heads, head_dim
-    // 128): in the launch it is 3-9 % faster for 1-4 sequences with q_len 4,
-    // 2-7 % for 1-16 sequences with q_len 1 and 1 % on the block-draft
+    // Measured against the merge kernel (per call; 32/8 heads, head_dim 128):
+    // in the launch it is 2-6 % faster for 1-4 sequences with q_len 4, 4-7 %
+    // for 1-8 sequences with q_len 1 (1 % at 16) and 1 % on the block-draft
     // workload (4 sequences, 64 rows).  With 1,024 merge wavefronts (8
     // sequences with q_len 4, the MTP workload) it was 1-2 % slower, and so
     // was it with 2-4 pieces per unit (64-128 sequences), hence the bounds.
