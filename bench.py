@@ -167,6 +167,7 @@ def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30, 
     t, pools = make_pools(wl, n_pools)
     shape = binding.shape_of(t["q"], t["k_pages"], t["page_table"], wl.max_ctx_len)
     ws = binding.new_workspace(binding.workspace_size(shape))
+    plan = binding.decode_attn_plan(shape)
     ev = [(binding.Event(), binding.Event()) for _ in range(steps)]
     sampled = range(0, steps, EVENT_EVERY)   # timed calls that carry kernel events
 
@@ -237,7 +238,19 @@ def time_workload(name, steps, warmup, min_warmup_ms=0.0, min_rotation=4 << 30, 
                 kv_gbps=kv / (ms_step * 1e-3) / 1e9,
                 kernel_gbps=alg / (kern_ms.mean() * 1e-3) / 1e9,
                 query_tokens_per_s=qtok / (ms_step * 1e-3), tokens_per_s=wl.B / (ms_step * 1e-3),
-                n_pools=n_pools, wl=wl, out_f64=out_f64, **extra)
+                n_pools=n_pools, plan=plan_summary(plan), wl=wl, out_f64=out_f64, **extra)
+
+
+PLAN_KERNEL = {1: "single-wavefront matrix-core", 2: "team of four wavefronts", 3: "VALU"}
+PLAN_COMBINE = {0: "merge kernel after the launch", 1: "last arriver in the launch",
+                2: "merge wavefronts in the launch"}
+
+
+def plan_summary(plan):
+    """What the timed call launched (ts_decode_attn_plan): kernel, workers,
+    how its splits were combined, workgroups of the streaming launch."""
+    return dict(kernel=PLAN_KERNEL.get(plan["variant"], str(plan["variant"])), workers=plan["num_workers"],
+                combine=PLAN_COMBINE.get(plan["combine"], str(plan["combine"])), grid=plan["grid"])
 
 
 def parity_errors(got, ref):
@@ -715,7 +728,7 @@ def main():
                      "kernel_ms_median": round(bulk["kernel_ms_median"], 5),
                      "kernel_ms_p10": round(bulk["kernel_ms_p10"], 5),
                      "kernel_ms_p90": round(bulk["kernel_ms_p90"], 5),
-                     "alg_bytes_per_launch": bulk["alg_bytes"]},
+                     "alg_bytes_per_launch": bulk["alg_bytes"], "plan": bulk["plan"]},
         "cpu_baseline": cpu,
         "ceiling": ceiling_summary(bulk),
         "paper_context": {"routing_only_speedup_max": 1.67, "routing_plus_speculation_speedup_max": 2.59,

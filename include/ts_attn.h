@@ -64,7 +64,7 @@
 extern "C" {
 #endif
 
-#define TS_ATTN_ABI_VERSION 3
+#define TS_ATTN_ABI_VERSION 4
 
 typedef enum ts_status {
     TS_OK = 0,
@@ -141,6 +141,32 @@ int ts_decode_attn_events(const ts_attn_shape *shape, const void *q, const void 
                           const int32_t *ctx_lens, const int32_t *q_lens, void *out,
                           float scale, void *workspace, size_t workspace_bytes, void *stream,
                           void *ev_begin, void *ev_end);
+
+/* What ts_decode_attn launches for `shape` on the current device, for
+ * diagnostics and tests: nothing is launched and no device memory is read.
+ * Splits of a unit (sequence, KV head) that several workers share are
+ * combined by the last worker to finish a piece of it, by merge wavefronts
+ * that follow the workers in the same launch, or by a separate merge kernel;
+ * the choice and the worker count depend on the shape and on the compiled
+ * kernels' occupancy.  Fills *plan; returns TS_OK or a negative ts_status
+ * (as ts_decode_attn would for the same shape). */
+#define TS_COMBINE_MERGE_KERNEL 0
+#define TS_COMBINE_LAST_ARRIVER 1
+#define TS_COMBINE_IN_LAUNCH 2
+
+typedef struct ts_attn_plan {
+    int32_t variant;            /* kernel used: TS_VARIANT_WAVE, _TEAM or _VALU */
+    int32_t num_workers;        /* workers of the page partition */
+    int32_t combine;            /* TS_COMBINE_* */
+    int32_t grid;               /* workgroups of the streaming launch (workers, then any
+                                   merge workgroups) */
+    int32_t threads;            /* threads per workgroup of the streaming launch */
+    int32_t merge_blocks;       /* workgroups of the merge kernel (0 if none runs) */
+    int64_t lds_bytes;          /* dynamic LDS per workgroup of the streaming launch */
+    int64_t workspace_bytes;    /* ts_decode_attn_workspace_size(shape) */
+} ts_attn_plan;
+
+int ts_decode_attn_plan(const ts_attn_shape *shape, ts_attn_plan *plan);
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc):

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(HERE, "libtsattn.so")
 # TS_ATTN_ABI_VERSION of the header these structures mirror: a library built
 # from another version may lay its structures out differently, so loading
 # one is refused.
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 TS_OK = 0
 STATUS = {0: "TS_OK", -1: "TS_ERR_NULL", -2: "TS_ERR_SHAPE", -3: "TS_ERR_WORKSPACE",
@@ -37,6 +37,13 @@ class AttnShape(ctypes.Structure):
 
 
 VARIANT_AUTO, VARIANT_WAVE, VARIANT_TEAM, VARIANT_VALU = 0, 1, 2, 3
+COMBINE_MERGE_KERNEL, COMBINE_LAST_ARRIVER, COMBINE_IN_LAUNCH = 0, 1, 2
+
+
+class AttnPlan(ctypes.Structure):
+    _fields_ = [("variant", ctypes.c_int32), ("num_workers", ctypes.c_int32), ("combine", ctypes.c_int32),
+                ("grid", ctypes.c_int32), ("threads", ctypes.c_int32), ("merge_blocks", ctypes.c_int32),
+                ("lds_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64)]
 
 
 class SweepConfig(ctypes.Structure):
@@ -59,6 +66,7 @@ class SweepPoint(ctypes.Structure):
 
 
 EXPORTS = ["ts_decode_attn_workspace_size", "ts_decode_attn", "ts_decode_attn_events", "ts_decode_attn_noalloc",
+           "ts_decode_attn_plan",
            "ts_concurrency_sweep", "ts_synth_fill_bf16", "ts_synth_sweep_lengths",
            "ts_synth_page_table", "ts_copy_bytes", "ts_stream_read", "ts_page_gather_read", "ts_event_create", "ts_event_destroy",
            "ts_event_record", "ts_event_elapsed_ms", "ts_status_string", "ts_last_error",
@@ -119,6 +127,8 @@ def _load() -> ctypes.CDLL:
     lib.ts_step_makespan.restype = ctypes.c_int
     lib.ts_decode_attn_noalloc.argtypes = [pshape, P, P, P, P, P, P, P, ctypes.c_float, P]
     lib.ts_decode_attn_noalloc.restype = ctypes.c_int
+    lib.ts_decode_attn_plan.argtypes = [pshape, ctypes.POINTER(AttnPlan)]
+    lib.ts_decode_attn_plan.restype = ctypes.c_int
     lib.ts_kv_append.argtypes = [pshape, P, P, P, P, P, P, P, P]
     lib.ts_kv_append.restype = ctypes.c_int
     lib.ts_spec_accept_workspace_size.argtypes = [I32, I32]
@@ -163,6 +173,14 @@ def workspace_size(shape: AttnShape) -> int:
     if n == 0:
         raise TsError(-2, "ts_decode_attn_workspace_size")
     return int(n)
+
+
+def decode_attn_plan(shape: AttnShape) -> dict:
+    """What ts_decode_attn launches for `shape` on the current device
+    (kernel, workers, how splits are combined, launch sizes)."""
+    plan = AttnPlan()
+    check(lib.ts_decode_attn_plan(ctypes.byref(shape), ctypes.byref(plan)), "ts_decode_attn_plan")
+    return {f: getattr(plan, f) for f, _ in AttnPlan._fields_}
 
 
 def _stream_ptr(stream) -> int:

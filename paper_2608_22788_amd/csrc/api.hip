@@ -226,6 +226,107 @@ static bool debug_enabled() {
     return v == 1;
 }
 
+// Everything a call launches, decided from the shape and the device.
+struct Launch {
+    kernel_fn main_k = nullptr;   // the streaming kernel
+    kernel_fn merge_k = nullptr;  // the merge kernel (kCombineKernel only)
+    size_t lds = 0;               // dynamic LDS of the merge kernel (the partition prefix)
+    size_t main_lds = 0;          // dynamic LDS of the streaming kernel
+    int main_threads = kWave;
+    unsigned grid = 0;            // workgroups of the streaming launch: workers, then merge ones
+    int combine = kCombineKernel;
+    int cnt_shift = 0;
+    int ws_o_bytes = 0;
+    int64_t merge_blocks = 0;     // workgroups of the merge kernel
+};
+
+// Completes a plan for the current device: kernel, worker count, how the
+// splits are combined and the launch sizes.  Launches nothing.
+static int finish_plan(const ts_attn_shape *s, Plan &pl, Launch &L) {
+    int st = check_device();
+    if (st)
+        return st;
+    const int B = s->num_seqs, Hkv = s->num_kv_heads, D = s->head_dim;
+    L.lds = (size_t)(B + 1) * sizeof(int);
+    L.main_lds = L.lds;
+    L.main_threads = kWave;
+    if (pl.q1) {
+        L.main_k = decode_q1_variant(D, pl.G);
+    } else if (pl.team) {
+        int extra = 0, nbe = 0;
+        L.main_k = verify_team_variant(pl.rows_per_unit, &extra, &nbe);
+        L.main_lds = ((L.lds + 15) & ~(size_t)15) + (size_t)extra;
+        L.main_threads = 4 * kWave;
+    } else {
+        L.main_k = verify_variant(D, pl.NB);
+    }
+    if (!L.main_k || !merge_variant(D, false))
+        return fail(TS_ERR_UNSUPPORTED, "no kernel for head_dim %d, G %d, rows %d", D, pl.G, pl.rows_per_unit);
+    if (pl.auto_w) {
+        // one full round of resident workers (the workspace is sized for pl.W)
+        const int resident = resident_workers(L.main_k, L.main_threads, L.main_lds);
+        if (resident > 0 && resident < pl.W)
+            pl.W = resident;
+    }
+    // Who combines the splits (attn_split.h):
+    //  * the last worker of a unit, for the single-wavefront kernels with at
+    //    least twice as many units as workers (a unit has one or two pieces);
+    //  * merge wavefronts appended to the grid, one per row of each unit, when
+    //    units have many pieces (a unit meets about W / units + 1 workers;
+    //    here W >= 8 units) and that takes at most kMaxMergeWgs workgroups;
+    //  * otherwise the merge kernel after the launch, and always when the
+    //    partial area is too large for 32-bit buffer offsets.
+    // Measured against the merge kernel (per call; 32/8 heads, head_dim 128):
+    // in the launch it is 2-6 % faster for 1-4 sequences with q_len 4, 4-7 %
+    // for 1-8 sequences with q_len 1 (1 % at 16) and 1 % on the block-draft
+    // workload (4 sequences, 64 rows).  With 1,024 merge wavefronts (8
+    // sequences with q_len 4, the MTP workload) it was 1-2 % slower, and so
+    // was it with 2-4 pieces per unit (64-128 sequences), hence the bounds.
+    constexpr int64_t kMaxMergeWgs = 512;
+    const size_t o_bytes = pl.ws_lse_off - pl.ws_o_off;
+    const int64_t units = (int64_t)B * Hkv;
+    const int ngroups = (pl.rows_per_unit + 3) / 4;
+    const int64_t merge_wgs = units * (pl.team ? ngroups : pl.rows_per_unit);
+    L.combine = kCombineKernel;
+    if (o_bytes < ((size_t)1 << 31)) {
+        if (!pl.team && units >= 2 * (int64_t)pl.W)
+            L.combine = kCombineLast;
+        else if ((int64_t)pl.W >= 8 * units && merge_wgs <= kMaxMergeWgs)
+            L.combine = kCombineInLaunch;
+    }
+    L.ws_o_bytes = L.combine != kCombineKernel ? (int)o_bytes : 0;
+    // Counters of consecutive units up to 4 KiB apart (inside the counter
+    // area) when merge wavefronts poll them.
+    L.cnt_shift = 0;
+    if (L.combine == kCombineInLaunch)
+        while (L.cnt_shift < 10 && units << (L.cnt_shift + 1) <= kMaxUnits)
+            L.cnt_shift++;
+    L.grid = (unsigned)(pl.W + (L.combine == kCombineInLaunch ? merge_wgs : 0));
+    if (L.combine == kCombineInLaunch && pl.team && pl.auto_w) {
+        // Reserve enough LDS that only the workers' teams fit on a compute
+        // unit (their registers would allow one more): a merge workgroup then
+        // starts where a team has finished instead of polling beside two
+        // streaming teams from the start, which measured 1 % faster.
+        const size_t lds_cu = (size_t)160 * 1024;
+        const int teams = per_cu_bound(false, true, pl.rows_per_unit);
+        const size_t gate = ((lds_cu / teams + lds_cu / (teams + 1)) / 2) & ~(size_t)1023;
+        if (L.main_lds < gate)
+            L.main_lds = gate;
+    }
+    if (L.combine == kCombineKernel) {
+        // A unit meets about W / units + 1 workers.  Up to about three pieces
+        // a unit, one wavefront per 4 rows takes every piece itself (a fourth
+        // of the blocks); beyond that four wavefronts share each row group's
+        // pieces.  Measured: 1,024 units with 16-32 rows, 768-1,024 workers,
+        // 1.5-6 % faster per call; at 4 pieces a unit (32 skewed sequences)
+        // the long sequences' units made it 2 % slower, hence the bound.
+        const bool few = (int64_t)pl.W <= 2 * units;
+        L.merge_k = merge_variant(D, few);
+        L.merge_blocks = units * (few ? (ngroups + 3) / 4 : ngroups);
+    }
+    return TS_OK;
+}
+
 int launch_attn(const ts_attn_shape *s, const void *q, const void *k_pages, const void *v_pages,
                   const int32_t *page_table, const int32_t *ctx_lens, const int32_t *q_lens,
                   void *out, float scale, void *workspace, size_t workspace_bytes, void *stream,
@@ -246,7 +347,8 @@ int launch_attn(const ts_attn_shape *s, const void *q, const void *k_pages, cons
         return fail(TS_ERR_ARG, "misaligned pointer (workspace needs 256 B, tensors 16 B)");
     if (!std::isfinite(scale))
         return fail(TS_ERR_ARG, "scale is not finite");
-    st = check_device();
+    Launch L;
+    st = finish_plan(s, pl, L);
     if (st)
         return st;
     hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
@@ -279,105 +381,28 @@ int launch_attn(const ts_attn_shape *s, const void *q, const void *k_pages, cons
     p.G = pl.G;
     p.rows_per_unit = pl.rows_per_unit;
     p.W = pl.W;
+    p.ws_o_bytes = L.ws_o_bytes;
+    p.combine = (int16_t)L.combine;
+    p.cnt_shift = (int16_t)L.cnt_shift;
     p.scale_log2 = scale * 1.4426950408889634f;
-
-    const size_t lds = (size_t)(p.B + 1) * sizeof(int);
-    kernel_fn main_k = nullptr;
-    size_t main_lds = lds;
-    int main_threads = kWave;
-    if (pl.q1) {
-        main_k = decode_q1_variant(p.D, pl.G);
-    } else if (pl.team) {
-        int extra = 0, nbe = 0;
-        main_k = verify_team_variant(pl.rows_per_unit, &extra, &nbe);
-        main_lds = ((lds + 15) & ~(size_t)15) + (size_t)extra;
-        main_threads = 4 * kWave;
-    } else {
-        main_k = verify_variant(p.D, pl.NB);
-    }
-    kernel_fn merge_k = merge_variant(p.D, false);
-    if (!main_k || !merge_k)
-        return fail(TS_ERR_UNSUPPORTED, "no kernel for head_dim %d, G %d, rows %d", p.D, pl.G,
-                    pl.rows_per_unit);
-    if (pl.auto_w) {
-        // one full round of resident workers (the workspace is sized for pl.W)
-        const int resident = resident_workers(main_k, main_threads, main_lds);
-        if (resident > 0 && resident < pl.W)
-            pl.W = resident;
-        p.W = pl.W;
-    }
-    // Who combines the splits (attn_split.h):
-    //  * the last worker of a unit, for the single-wavefront kernels with at
-    //    least twice as many units as workers (a unit has one or two pieces);
-    //  * merge wavefronts appended to the grid, one per row of each unit, when
-    //    units have many pieces (a unit meets about W / units + 1 workers;
-    //    here W >= 8 units) and that takes at most kMaxMergeWgs workgroups;
-    //  * otherwise the merge kernel after the launch, and always when the
-    //    partial area is too large for 32-bit buffer offsets.
-    // Measured against the merge kernel (per call; 32/8 heads, head_dim 128):
-    // in the launch it is 2-6 % faster for 1-4 sequences with q_len 4, 4-7 %
-    // for 1-8 sequences with q_len 1 (1 % at 16) and 1 % on the block-draft
-    // workload (4 sequences, 64 rows).  With 1,024 merge wavefronts (8
-    // sequences with q_len 4, the MTP workload) it was 1-2 % slower, and so
-    // was it with 2-4 pieces per unit (64-128 sequences), hence the bounds.
-    constexpr int64_t kMaxMergeWgs = 512;
-    const size_t o_bytes = pl.ws_lse_off - pl.ws_o_off;
-    const int64_t units = (int64_t)p.B * p.Hkv;
-    const int ngroups = (pl.rows_per_unit + 3) / 4;
-    const int64_t merge_wgs = units * (pl.team ? ngroups : pl.rows_per_unit);
-    p.combine = kCombineKernel;
-    if (o_bytes < ((size_t)1 << 31)) {
-        if (!pl.team && units >= 2 * (int64_t)p.W)
-            p.combine = kCombineLast;
-        else if ((int64_t)p.W >= 8 * units && merge_wgs <= kMaxMergeWgs)
-            p.combine = kCombineInLaunch;
-    }
-    p.ws_o_bytes = p.combine != kCombineKernel ? (int)o_bytes : 0;
-    // Counters of consecutive units up to 4 KiB apart (inside the counter
-    // area) when merge wavefronts poll them.
-    p.cnt_shift = 0;
-    if (p.combine == kCombineInLaunch)
-        while (p.cnt_shift < 10 && units << (p.cnt_shift + 1) <= kMaxUnits)
-            p.cnt_shift++;
-    const unsigned grid = (unsigned)(p.W + (p.combine == kCombineInLaunch ? merge_wgs : 0));
-    if (p.combine == kCombineInLaunch && pl.team && pl.auto_w) {
-        // Reserve enough LDS that only the workers' teams fit on a compute
-        // unit (their registers would allow one more): a merge workgroup then
-        // starts where a team has finished instead of polling beside two
-        // streaming teams from the start, which measured 1 % faster.
-        const size_t lds_cu = (size_t)160 * 1024;
-        const int teams = per_cu_bound(false, true, pl.rows_per_unit);
-        const size_t gate = ((lds_cu / teams + lds_cu / (teams + 1)) / 2) & ~(size_t)1023;
-        if (main_lds < gate)
-            main_lds = gate;
-    }
 
     hipError_t e;
     if (ev_begin || ev_end) {
         // the events take the kernel's own start and end timestamps
         void *args[] = {&p};
-        e = hipExtLaunchKernel(reinterpret_cast<const void *>(main_k), dim3(grid), dim3(main_threads), args,
-                               main_lds, hs, reinterpret_cast<hipEvent_t>(ev_begin),
+        e = hipExtLaunchKernel(reinterpret_cast<const void *>(L.main_k), dim3(L.grid), dim3(L.main_threads), args,
+                               L.main_lds, hs, reinterpret_cast<hipEvent_t>(ev_begin),
                                reinterpret_cast<hipEvent_t>(ev_end), 0);
         if (e != hipSuccess)
             return hip_fail(e, "attention kernel launch");
     } else {
-        hipLaunchKernelGGL(main_k, dim3(grid), dim3(main_threads), main_lds, hs, p);
+        hipLaunchKernelGGL(L.main_k, dim3(L.grid), dim3(L.main_threads), L.main_lds, hs, p);
     }
     if ((e = hipGetLastError()) != hipSuccess)
         return hip_fail(e, "attention kernel launch");
-    if (p.combine != kCombineKernel)
+    if (L.combine != kCombineKernel)
         return TS_OK;   // the launch combined its own splits
-    // A unit meets about W / units + 1 workers.  Up to about three pieces a
-    // unit, one wavefront per 4 rows takes every piece itself (a fourth of
-    // the blocks); beyond that four wavefronts share each row group's pieces.
-    // Measured: 1,024 units with 16-32 rows, 768-1,024 workers, 1.5-6 %
-    // faster per call; at 4 pieces a unit (32 skewed sequences) the long
-    // sequences' units made it 2 % slower, hence the bound.
-    const bool few = (int64_t)p.W <= 2 * units;
-    const int64_t merge_blocks = units * (few ? (ngroups + 3) / 4 : ngroups);
-    hipLaunchKernelGGL(few ? merge_variant(p.D, true) : merge_k, dim3((unsigned)merge_blocks), dim3(4 * kWave), lds,
-                       hs, p);
+    hipLaunchKernelGGL(L.merge_k, dim3((unsigned)L.merge_blocks), dim3(4 * kWave), L.lds, hs, p);
     if ((e = hipGetLastError()) != hipSuccess)
         return hip_fail(e, "merge kernel launch");
     return TS_OK;
@@ -395,6 +420,35 @@ size_t ts_decode_attn_workspace_size(const ts_attn_shape *shape) {
     if (make_plan(shape, &pl))
         return 0;
     return pl.ws_bytes;
+}
+
+int ts_decode_attn_plan(const ts_attn_shape *shape, ts_attn_plan *plan) {
+    try {
+        clear_error();
+        if (!plan)
+            return fail(TS_ERR_NULL, "plan is NULL");
+        Plan pl;
+        int st = make_plan(shape, &pl);
+        if (st)
+            return st;
+        Launch L;
+        st = finish_plan(shape, pl, L);
+        if (st)
+            return st;
+        plan->variant = pl.q1 ? TS_VARIANT_VALU : pl.team ? TS_VARIANT_TEAM : TS_VARIANT_WAVE;
+        plan->num_workers = pl.W;
+        plan->combine = L.combine == kCombineLast       ? TS_COMBINE_LAST_ARRIVER
+                        : L.combine == kCombineInLaunch ? TS_COMBINE_IN_LAUNCH
+                                                        : TS_COMBINE_MERGE_KERNEL;
+        plan->grid = (int32_t)L.grid;
+        plan->threads = L.main_threads;
+        plan->merge_blocks = (int32_t)L.merge_blocks;
+        plan->lds_bytes = (int64_t)L.main_lds;
+        plan->workspace_bytes = (int64_t)pl.ws_bytes;
+        return TS_OK;
+    } catch (...) {
+        return fail(TS_ERR_HIP, "unexpected C++ exception");
+    }
 }
 
 int ts_decode_attn(const ts_attn_shape *shape, const void *q, const void *k_pages,

@@ -29,7 +29,7 @@ def test_exports_every_declared_function():
 
 
 def test_version_and_status_strings():
-    assert b.lib.ts_version() == b.ABI_VERSION == 3
+    assert b.lib.ts_version() == b.ABI_VERSION == 4
     for st in (0, -1, -2, -3, -4, -5, -6):
         assert b.lib.ts_status_string(st)
     assert b.lib.ts_status_string(-99) == b"unknown status"
@@ -55,6 +55,12 @@ def test_bad_shapes_rejected(kw):
     st = b.lib.ts_decode_attn(ctypes.byref(s), 16, 16, 16, 16, 16, 16, 16, ctypes.c_float(1.0),
                               256, 1 << 30, None)
     assert st == -2
+    assert b.lib.ts_decode_attn_plan(ctypes.byref(s), ctypes.byref(b.AttnPlan())) == -2
+
+
+def test_plan_needs_an_output():
+    assert b.lib.ts_decode_attn_plan(ctypes.byref(base_shape()), None) == -1
+    assert b"plan" in b.lib.ts_last_error()
 
 
 def test_variant_checks():

@@ -117,3 +117,13 @@ def test_parity_errors_over_valid_rows(bench):
     assert abs(p["max_abs"] - 0.1) < 1e-15 and abs(p["mean_abs"] - 0.1 / 12) < 1e-15
     norm = np.sqrt(1 + 4 + 0.25 + 8 * 0.0625)
     assert abs(p["rel_l2"] - 0.1 / norm) < 1e-15
+
+
+def test_plan_summary_names_the_launch():
+    import bench
+    got = bench.plan_summary(dict(variant=2, num_workers=512, combine=2, grid=1024, threads=256,
+                                  merge_blocks=0, lds_bytes=66560, workspace_bytes=1 << 20))
+    assert got == dict(kernel="team of four wavefronts", workers=512, combine="merge wavefronts in the launch",
+                       grid=1024)
+    assert bench.plan_summary(dict(variant=1, num_workers=1024, combine=1, grid=1024))["combine"] == \
+        "last arriver in the launch"

@@ -181,7 +181,7 @@ def test_in_kernel_combine_with_many_pieces(dev, orc, Qmax):
     """Skewed lengths so that units are plentiful (in-kernel combining is on:
     units >= 2 x workers) while one long sequence's units are each split over
     ~40 workers, more pieces than one combine batch holds."""
-    _, device = dev
+    binding, device = dev
     ctx = [50000] + [16 + (7 * b) % 40 for b in range(99)]
     q = [Qmax] * 100
     wl = synth.make_workload("manypieces", seed=21, cfg=small_cfg(32, 8, 128), ctx_lens=ctx, q_lens=q,
@@ -191,6 +191,9 @@ def test_in_kernel_combine_with_many_pieces(dev, orc, Qmax):
     for var in (0, 1, 3) if Qmax == 1 else (0, 1):
         for w in (300, 397):
             say(f"many pieces Qmax={Qmax} variant={var} workers={w}")
+            plan = binding.decode_attn_plan(binding.shape_of(t["q"], t["k_pages"], t["page_table"],
+                                                             wl.max_ctx_len, num_workers=w, variant=var))
+            assert plan["combine"] == binding.COMBINE_LAST_ARRIVER and plan["grid"] == w, plan
             t["out_full"].fill_(device.CANARY)
             device.run(wl, t, num_workers=w, variant=var)
             got = device.out_as_f64(t)
@@ -209,6 +212,9 @@ IN_LAUNCH = [
     ("team_q16", 32, 8, 128, [16, 5], [30000, 7000]),              # 64 rows: the team kernel
     ("d64_g8", 64, 8, 64, [2, 2], [12000, 16]),
 ]
+# variants whose plan is not the in-launch merge: 64 rows on one wavefront
+# need 16 units x 64 merge wavefronts, more than the launch takes
+NOT_IN_LAUNCH = {("team_q16", 1)}
 
 
 @pytest.mark.parametrize("case", IN_LAUNCH, ids=[c[0] for c in IN_LAUNCH])
@@ -230,6 +236,12 @@ def test_merge_in_the_launch(dev, orc, case):
     for var in variants_for(wl):
         for w in (0, 4096):
             say(f"in-launch merge {name} variant={var} workers={w}")
+            plan = binding.decode_attn_plan(binding.shape_of(t["q"], t["k_pages"], t["page_table"],
+                                                             max(1, wl.max_ctx_len), num_workers=w, variant=var))
+            want = binding.COMBINE_MERGE_KERNEL if (name, var) in NOT_IN_LAUNCH else binding.COMBINE_IN_LAUNCH
+            assert plan["combine"] == want, plan
+            if want == binding.COMBINE_IN_LAUNCH:
+                assert plan["grid"] > plan["num_workers"] and plan["merge_blocks"] == 0, plan
             t["out_full"].fill_(device.CANARY)
             device.run(wl, t, num_workers=w, variant=var, workspace=ws)
             got = device.out_as_f64(t)
