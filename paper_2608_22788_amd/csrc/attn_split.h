@@ -10,8 +10,9 @@
 //
 // Lane layout of a combining wavefront: lane (row, part) = 16 * row + part
 // owns dims VE * part .. VE * part + VE - 1 (VE = D / 16) of row `row` of a
-// group of 4 rows.  Partials are loaded kMergeBatch at a time, all loads
-// issued before any is consumed.
+// group of 4 rows.  Partials are loaded kMergeBatch at a time (4 in the
+// streaming kernels' own combine, whose registers are shared with the page
+// pipeline), all loads issued before any is consumed.
 #pragma once
 
 #include "attn_common.h"
@@ -112,15 +113,15 @@ struct Acc {
         den = 0.0f;
         M = -INFINITY;
     }
-    // Adds a batch of up to kMergeBatch partials (n valid) given their rows.
+    // Adds a batch of up to kB partials (n valid) given their rows.
     // kCoherent: read them with device-coherent loads (partials written by
     // other workers of the same launch), else with plain vector loads.
-    template <int D, bool kCoherent>
+    template <int D, bool kCoherent, int kB>
     __device__ void add_batch(const AttnParams &p, const size_t *rows, int n, int part) {
-        float l[kMergeBatch];
-        float4 v[kMergeBatch][VE / 4];
+        float l[kB];
+        float4 v[kB][VE / 4];
 #pragma unroll
-        for (int k = 0; k < kMergeBatch; k++) {
+        for (int k = 0; k < kB; k++) {
             const size_t row = rows[k < n ? k : 0];
             const float *src = p.ws_o + row * D + VE * part;
             if constexpr (kCoherent) {
@@ -139,13 +140,13 @@ struct Acc {
         }
         float Mb = M;
 #pragma unroll
-        for (int k = 0; k < kMergeBatch; k++)
+        for (int k = 0; k < kB; k++)
             Mb = fmaxf(Mb, l[k]);
         if (Mb == -INFINITY)
             return;
         rescale(Mb);
 #pragma unroll
-        for (int k = 0; k < kMergeBatch; k++) {
+        for (int k = 0; k < kB; k++) {
             const float wt = l[k] == -INFINITY ? 0.0f : fast_exp2(l[k] - M);
             den += wt;
 #pragma unroll
@@ -167,21 +168,22 @@ struct Acc {
     }
 };
 
-// Adds to `a` the partials k = k0, k0 + kstep, ... of row rr of the unit.
-template <int D, bool kCoherent>
+// Adds to `a` the partials k = k0, k0 + kstep, ... of row rr of the unit,
+// kB at a time.
+template <int D, bool kCoherent, int kB = kMergeBatch>
 __device__ void gather_partials(const AttnParams &p, const UnitSplit &u, size_t rr, int part,
                                 int k0, int kstep, Acc<D / 16> &a) {
     const size_t R = p.rows_per_unit;
-    for (int kb = k0; kb < u.nparts; kb += kstep * kMergeBatch) {
-        size_t rows[kMergeBatch];
+    for (int kb = k0; kb < u.nparts; kb += kstep * kB) {
+        size_t rows[kB];
         int n = 0;
 #pragma unroll
-        for (int k = 0; k < kMergeBatch; k++) {
+        for (int k = 0; k < kB; k++) {
             const int kk = kb + kstep * k;
             rows[k] = (size_t)u.slot(kk < u.nparts ? kk : kb) * R + rr;
             n += kk < u.nparts;
         }
-        a.template add_batch<D, kCoherent>(p, rows, n, part);
+        a.template add_batch<D, kCoherent, kB>(p, rows, n, part);
     }
 }
 
@@ -217,7 +219,7 @@ __device__ void combine_unit(const AttnParams &p, int b, int g, const UnitSplit 
         const bool row_ok = r < R && r / p.G < Q;
         Acc<D / 16> a;
         a.init();
-        gather_partials<D, true>(p, u, row_ok ? r : 0, part, 0, 1, a);
+        gather_partials<D, true, 4>(p, u, row_ok ? r : 0, part, 0, 1, a);
         if (row_ok)
             write_merged<D>(p, b, g, r, part, a);
     }

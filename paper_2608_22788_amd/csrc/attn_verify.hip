@@ -27,8 +27,12 @@
 //     untouched on almost every page;
 //   * the next page is loaded into a second register set while the current
 //     one is computed; loads go through a buffer resource bounded to the
-//     page's block, so a prefetch past the segment end reads nothing (it used
-//     to re-read the last page: about 0.8 % of the bulk call's traffic).
+//     page's block, so a prefetch past the end reads nothing (it used to
+//     re-read the last page: about 0.8 % of the bulk call's traffic).  With
+//     one row block the prefetch runs on across the end of a segment into
+//     the next segment's first page, whose lengths and query rows are
+//     fetched when the current segment starts, so the pipeline is not
+//     drained at a unit boundary.
 // Masks: key t is visible to draft row i iff t <= L - Q + i; keys past the
 // segment end or the context end get probability 0 and their value rows are
 // zeroed before the product, so stale data never reaches the output.
@@ -79,12 +83,10 @@ struct Verify {
         VRow<VE> v[4];      // value rows of the lane's 4 tokens
     };
 
-    // Page j of the segment [.., j1); past the segment the loads are no-ops
-    // that yield zeros (the page is then computed fully masked).
-    __device__ static void load_page(const AttnParams &p, const int32_t *pt, int j, int j1, int g, int n,
-                                     int kq, PageRegs &r) {
-        const bool in = j < j1;
-        const int pid = ld_meta(pt, in ? j : j1 - 1);
+    // The K and V blocks of KV head g in physical page pid.  With !in the
+    // buffer resources hold no records: the loads return zeros and touch no
+    // memory, so a prefetch past the worker's range needs no branch.
+    __device__ static void load_block(const AttnParams &p, int pid, bool in, int g, int n, int kq, PageRegs &r) {
         const size_t base = ((size_t)pid * p.Hkv + g) * (size_t)(kPage * D);
         const block_rsrc_t rk = block_rsrc(p.k_pages + base, in ? kBlockBytes : 0);
         const block_rsrc_t rv = block_rsrc(p.v_pages + base, in ? kBlockBytes : 0);
@@ -175,56 +177,64 @@ struct Verify {
         }
     }
 
-    __device__ static void segment(const AttnParams &p, const Segment &s, int slot_id, int64_t ptot) {
-        const int lane = threadIdx.x;
-        const int n = lane & 15;
-        const int kq = lane >> 4;
-        const int b = s.b, g = s.g;
-        const int G = p.G;
-        const int L = ld_meta(p.ctx_lens, b);
-        const int Q = ld_meta(p.q_lens, b);
-        const int R = p.rows_per_unit;
-        const int32_t *pt = p.page_table + (size_t)b * p.max_pages;
-        const int seg_end_tok = min(L, s.j1 * kPage);
+    // The segment being computed, with its lengths and masks.
+    struct Cur {
+        Segment s;
+        const int32_t *pt;   // the sequence's page-table row
+        int L, Q;
+        int seg_end_tok, full_end;
+    };
 
-        State st;
+    __device__ static void head(const AttnParams &p, const Segment &s, Cur &c) {
+        c.s = s;
+        c.pt = p.page_table + (size_t)s.b * p.max_pages;
+        c.L = ld_meta(p.ctx_lens, s.b);
+        c.Q = ld_meta(p.q_lens, s.b);
+    }
+
+    // Query rows of unit (b, g) in the lane's B-operand layout.  Rows past
+    // R = G * Qmax read row R - 1 (inside q); start() zeroes every row that
+    // is not a draft row of the sequence.
+    __device__ static void load_q(const AttnParams &p, int b, int g, int n, int kq, uint4 (&q)[NB][KS]) {
+        const int G = p.G, R = p.rows_per_unit;
+#pragma unroll
+        for (int rb = 0; rb < NB; rb++) {
+            const int rc = min(rb * 16 + n, R - 1);
+            const uint16_t *qr = p.q + (((size_t)b * p.Qmax + rc / G) * p.Hq + (size_t)g * G + rc % G) * D + 8 * kq;
+#pragma unroll
+            for (int ks = 0; ks < KS; ks++)
+                q[rb][ks] = *reinterpret_cast<const uint4 *>(qr + 32 * ks);
+        }
+    }
+
+    // Masks and empty accumulators for segment c.
+    __device__ static void start(const AttnParams &p, Cur &c, const uint4 (&q)[NB][KS], State &st, int n) {
+        const int G = p.G, R = p.rows_per_unit, L = c.L, Q = c.Q;
+        c.seg_end_tok = min(L, c.s.j1 * kPage);
+        // keys below this bound are visible to every row of the block
+        c.full_end = min(L - Q + 1, c.seg_end_tok);
 #pragma unroll
         for (int rb = 0; rb < NB; rb++) {
             const int r = rb * 16 + n;
             const bool row_ok = r < R && r / G < Q;
-            const int i = row_ok ? r / G : 0;
-            const int hl = row_ok ? r % G : 0;
-            st.lim[rb] = min(row_ok ? L - Q + i + 1 : L, seg_end_tok);
-            const uint16_t *qr = p.q + (((size_t)b * p.Qmax + i) * p.Hq + (size_t)g * G + hl) * D + 8 * kq;
+            st.lim[rb] = min(row_ok ? L - Q + r / G + 1 : L, c.seg_end_tok);
 #pragma unroll
             for (int ks = 0; ks < KS; ks++)
-                st.qf[rb][ks] = row_ok ? *reinterpret_cast<const uint4 *>(qr + 32 * ks) : make_uint4(0, 0, 0, 0);
+                st.qf[rb][ks] = row_ok ? q[rb][ks] : make_uint4(0, 0, 0, 0);
             st.m_ref[rb] = -INFINITY;
             st.lacc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int jj = 0; jj < VE; jj++)
                 st.acc[rb][jj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
-        // keys below this bound are visible to every row of the block
-        const int full_end = min(L - Q + 1, seg_end_tok);
+    }
 
-        // Prefetches are issued unconditionally: a page past the segment is
-        // loaded through a buffer resource with no records (zeros, no memory
-        // access), so no load sits under a branch.
-        constexpr int kRing = 2;
-        PageRegs ring[kRing];
-        load_page(p, pt, s.j0, s.j1, g, n, kq, ring[0]);
-        for (int j = s.j0; j < s.j1; j += kRing) {
-#pragma unroll
-            for (int k = 0; k < kRing; k++) {
-                if (j + k < s.j1) {
-                    load_page(p, pt, j + k + kRing - 1, s.j1, g, n, kq, ring[(k + kRing - 1) % kRing]);
-                    page_step(p, st, ring[k], j + k, full_end, seg_end_tok, kq);
-                }
-            }
-        }
-
-        // epilogue: lane holds rows 16 rb + 4 kq + i, dims VE n .. VE n + VE - 1
+    // Writes segment c's rows: to `out` when the segment is its whole unit,
+    // else as a normalised partial with its log2-sum-exp in slot slot_id.
+    __device__ static void finish(const AttnParams &p, const Cur &c, const State &st, int slot_id, int64_t ptot,
+                                  int n, int kq) {
+        const int b = c.s.b, g = c.s.g, G = p.G, R = p.rows_per_unit, Q = c.Q;
+        // lane holds rows 16 rb + 4 kq + i, dims VE n .. VE n + VE - 1
 #pragma unroll
         for (int rb = 0; rb < NB; rb++) {
 #pragma unroll
@@ -236,7 +246,7 @@ struct Verify {
                 if (r >= R || di >= Q)
                     continue;
                 const float inv = l > 0.0f ? 1.0f / l : 0.0f;
-                if (s.whole) {
+                if (c.s.whole) {
                     uint16_t *dst = p.out + (((size_t)b * p.Qmax + di) * p.Hq + (size_t)g * G + r % G) * D + VE * n;
                     uint32_t w[VE / 2];
 #pragma unroll
@@ -271,8 +281,111 @@ struct Verify {
                 }
             }
         }
-        if (!s.whole && p.combine == kCombineLast)
-            arrive_and_combine<D>(p, s, ptot, lane);
+        if (!c.s.whole && p.combine == kCombineLast)
+            arrive_and_combine<D>(p, c.s, ptot, threadIdx.x);
+    }
+
+    // One segment on its own, the page after the current one in flight
+    // within the segment (the layout for two or more row blocks, which have
+    // no registers to spare for a pipeline across segments).
+    __device__ static void segment(const AttnParams &p, const Segment &s, int slot_id, int64_t ptot) {
+        const int lane = threadIdx.x;
+        const int n = lane & 15;
+        const int kq = lane >> 4;
+        const int G = p.G, R = p.rows_per_unit;
+        Cur c;
+        head(p, s, c);
+        c.seg_end_tok = min(c.L, s.j1 * kPage);
+        c.full_end = min(c.L - c.Q + 1, c.seg_end_tok);
+        State st;
+#pragma unroll
+        for (int rb = 0; rb < NB; rb++) {
+            const int r = rb * 16 + n;
+            const bool row_ok = r < R && r / G < c.Q;
+            const int i = row_ok ? r / G : 0;
+            const int hl = row_ok ? r % G : 0;
+            st.lim[rb] = min(row_ok ? c.L - c.Q + i + 1 : c.L, c.seg_end_tok);
+            const uint16_t *qr = p.q + (((size_t)s.b * p.Qmax + i) * p.Hq + (size_t)s.g * G + hl) * D + 8 * kq;
+#pragma unroll
+            for (int ks = 0; ks < KS; ks++)
+                st.qf[rb][ks] = row_ok ? *reinterpret_cast<const uint4 *>(qr + 32 * ks) : make_uint4(0, 0, 0, 0);
+            st.m_ref[rb] = -INFINITY;
+            st.lacc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int jj = 0; jj < VE; jj++)
+                st.acc[rb][jj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+        PageRegs ring[2];
+        load_block(p, ld_meta(c.pt, s.j0), true, s.g, n, kq, ring[0]);
+        for (int j = s.j0; j < s.j1; j += 2) {
+#pragma unroll
+            for (int k = 0; k < 2; k++) {
+                if (j + k < s.j1) {
+                    const bool in = j + k + 1 < s.j1;
+                    load_block(p, ld_meta(c.pt, in ? j + k + 1 : s.j1 - 1), in, s.g, n, kq, ring[1 - k]);
+                    page_step(p, st, ring[k], j + k, c.full_end, c.seg_end_tok, kq);
+                }
+            }
+        }
+        finish(p, c, st, slot_id, ptot, n, kq);
+    }
+
+    // Streams the worker's global pages [begin, end) with one row block as
+    // one pipeline: the page after the current one is always in flight, also
+    // across the end of a segment, where it is the next segment's first page.
+    // The next segment is located, its lengths read and its query rows
+    // loaded when the current one starts, so a unit boundary costs the
+    // epilogue and no refill of the pipeline.
+    __device__ static void run(const AttnParams &p, const int *s_pre, int64_t begin, int64_t end, int w,
+                               int64_t ptot, Arrivals &arr) {
+        const int lane = threadIdx.x;
+        const int n = lane & 15;
+        const int kq = lane >> 4;
+        Cur c, nx;
+        head(p, locate(p, s_pre, begin, end), c);
+        uint4 q[NB][KS];
+        load_q(p, c.s.b, c.s.g, n, kq, q);
+        PageRegs ring[2];
+        load_block(p, ld_meta(c.pt, c.s.j0), true, c.s.g, n, kq, ring[0]);
+        bool more = c.s.next < end;
+        State st;
+        start(p, c, q, st, n);
+        if (more) {
+            head(p, locate(p, s_pre, c.s.next, end), nx);
+            load_q(p, nx.s.b, nx.s.g, n, kq, q);
+        }
+        int slot_id = 2 * w;
+        int j = c.s.j0;
+        while (true) {
+#pragma unroll
+            for (int k = 0; k < 2; k++) {
+                // The next page of the range goes into the other ring slot,
+                // loaded unconditionally (after the range's last page: nothing).
+                const bool last = j + 1 == c.s.j1;
+                const bool to_next = last && more;
+                const int32_t *tpt = to_next ? nx.pt : c.pt;
+                const int tj = to_next ? nx.s.j0 : min(j + 1, c.s.j1 - 1);
+                load_block(p, ld_meta(tpt, tj), !last || more, to_next ? nx.s.g : c.s.g, n, kq, ring[1 - k]);
+                page_step(p, st, ring[k], j, c.full_end, c.seg_end_tok, kq);
+                if (last) {
+                    finish(p, c, st, slot_id, ptot, n, kq);
+                    arr.add(p, c.s);
+                    if (!more)
+                        return;
+                    slot_id = 2 * w + 1;
+                    c = nx;
+                    j = c.s.j0;
+                    more = c.s.next < end;
+                    start(p, c, q, st, n);
+                    if (more) {
+                        head(p, locate(p, s_pre, c.s.next, end), nx);
+                        load_q(p, nx.s.b, nx.s.g, n, kq, q);
+                    }
+                } else {
+                    j++;
+                }
+            }
+        }
     }
 };
 
@@ -291,11 +404,16 @@ __global__ __launch_bounds__(64) void verify_kernel(AttnParams p) {
     const int64_t end = worker_begin(ptot, w + 1, p.W);
     Arrivals arr;
     arr.init();
-    for (int64_t x = begin; x < end;) {
-        const Segment s = locate(p, s_pre, x, end);
-        Verify<D, NB>::segment(p, s, x == begin ? 2 * w : 2 * w + 1, ptot);
-        arr.add(p, s);
-        x = s.next;
+    if constexpr (NB == 1) {
+        if (begin < end)
+            Verify<D, NB>::run(p, s_pre, begin, end, w, ptot, arr);
+    } else {
+        for (int64_t x = begin; x < end;) {
+            const Segment s = locate(p, s_pre, x, end);
+            Verify<D, NB>::segment(p, s, x == begin ? 2 * w : 2 * w + 1, ptot);
+            arr.add(p, s);
+            x = s.next;
+        }
     }
     arr.flush<false>(p);
 }
