@@ -153,6 +153,49 @@ def test_many_sequences(dev, orc, B, Qmax):
     run_case(dev, orc, wl, workers=(0, 5, 2000))
 
 
+def test_random_worker_counts_every_combine_mode(dev, orc):
+    """Random shapes (a third of them a few long sequences, so units hold many
+    pieces) at the automatic and at a random worker count, every variant,
+    one workspace for all calls: every output element against the oracle,
+    the canaries untouched, the counter area zero after each call, and each
+    of the three ways of combining splits taken at least once."""
+    import torch
+    binding, device = dev
+    ws = binding.new_workspace(640 << 20)
+    seen = set()
+    for seed in range(36):
+        rng = np.random.default_rng(7000 + seed)
+        sh = random_shape(seed + 5000)
+        if seed % 3 == 0:
+            Hkv = int(rng.choice([1, 2, 8]))
+            Qmax = int(rng.choice([1, 2, 4, 8, 16]))
+            G = int(rng.choice([g for g in (1, 2, 4, 8) if g * Qmax <= 64]))
+            ql = [int(x) for x in rng.integers(1, Qmax + 1, size=int(rng.integers(1, 4)))]
+            ql[0] = Qmax
+            sh = dict(Hq=G * Hkv, Hkv=Hkv, D=int(rng.choice([64, 128])), Qmax=Qmax, q_lens=ql,
+                      ctx_lens=[int(max(q, rng.integers(1000, 30000))) for q in ql])
+        wl = synth.make_workload(f"modes{seed}", seed=seed, cfg=small_cfg(sh["Hq"], sh["Hkv"], sh["D"]),
+                                 ctx_lens=sh["ctx_lens"], q_lens=sh["q_lens"], Qmax=sh["Qmax"], poison=True,
+                                 spare_pages=1)
+        ref = oracle_out(orc, wl, nthreads=8)
+        t = device.upload(wl)
+        for var in variants_for(wl):
+            for w in (0, int(rng.choice([1, 7, 64, 333, 1024, 2048, 4096]))):
+                plan = binding.decode_attn_plan(binding.shape_of(t["q"], t["k_pages"], t["page_table"],
+                                                                 max(1, wl.max_ctx_len), num_workers=w,
+                                                                 variant=var))
+                seen.add(plan["combine"])
+                say(f"modes seed={seed} B={wl.B} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} Qmax={wl.Qmax} "
+                    f"variant={var} workers={w} combine={plan['combine']}")
+                t["out_full"].fill_(device.CANARY)
+                device.run(wl, t, num_workers=w, variant=var, workspace=ws)
+                assert_parity(device.out_as_f64(t), ref, f"modes{seed} v{var} w{w}")
+                canary_ok(t, wl)
+                torch.cuda.synchronize()
+                assert int(ws[:1 << 20].count_nonzero()) == 0, f"counters left set: seed {seed} v{var} w{w}"
+    assert seen == {binding.COMBINE_MERGE_KERNEL, binding.COMBINE_LAST_ARRIVER, binding.COMBINE_IN_LAUNCH}, seen
+
+
 def test_workspace_reused_across_calls_and_shapes(dev, orc):
     """One zero-filled workspace serves a run of calls of different shapes and
     worker counts; each result matches the oracle, and after every call the
