@@ -341,8 +341,9 @@ struct Verify {
         const int lane = threadIdx.x;
         const int n = lane & 15;
         const int kq = lane >> 4;
-        Cur c, nx;
+        Cur c;
         head(p, locate(p, s_pre, begin, end), c);
+        Cur nx = c;   // the next segment, once there is one
         uint4 q[NB][KS];
         load_q(p, c.s.b, c.s.g, n, kq, q);
         PageRegs ring[2];
