@@ -179,3 +179,31 @@ def test_accept_golden_cases():
     n, t = run_accept(p, q, d, nd, ua, us)
     for b, c in enumerate(cases):
         assert [int(n[b]), int(t[b])] == c["want"], f'{c["name"]}: {[int(n[b]), int(t[b])]} vs {c["want"]}'
+
+
+def test_accept_one_workspace_for_many_calls():
+    """One workspace, never cleared, serves calls of different batch sizes
+    and vocabularies in turn: every result equals the oracle's (the
+    workspace's contents on entry do not matter)."""
+    import torch
+    from paper_2608_22788_amd import binding
+    big = int(binding.lib.ts_spec_accept_workspace_size(64, 151936))
+    ws = torch.full((big,), 0x5A, dtype=torch.uint8, device="cuda")
+    t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dtype=dt, device="cuda")  # noqa: E731
+    for n, (V, G, B) in enumerate([(151936, 4, 8), (1001, 3, 9), (151936, 15, 64), (50, 2, 3), (32000, 6, 17)]):
+        rng = np.random.default_rng(500 + n)
+        p, logits = probs(rng, B, G + 1, V, 2.0)
+        q, _ = probs(rng, B, G, V, 0, base=logits[:, :G], noise=0.5)
+        d = np.stack([[rng.choice(V, p=q[b, i].astype(np.float64) / q[b, i].astype(np.float64).sum())
+                       for i in range(G)] for b in range(B)]).astype(np.int32)
+        nd = rng.integers(0, G + 1, size=B).astype(np.int32)
+        ua = rng.random((B, G)).astype(np.float32)
+        us = rng.random(B).astype(np.float32)
+        say(f"accept reuse {n}: V={V} G={G} B={B}")
+        na = torch.full((B,), -1, dtype=torch.int32, device="cuda")
+        nt = torch.full((B,), -1, dtype=torch.int32, device="cuda")
+        binding.spec_accept(t(p, torch.float32), t(q, torch.float32), t(d, torch.int32), t(nd, torch.int32),
+                            t(ua, torch.float32), t(us, torch.float32), na, nt, workspace=ws)
+        torch.cuda.synchronize()
+        n_ref, t_ref = sd.spec_accept(p, q, d, nd, ua, us)
+        assert np.array_equal(na.cpu().numpy(), n_ref) and np.array_equal(nt.cpu().numpy(), t_ref), f"call {n}"
