@@ -557,6 +557,36 @@ def ceiling_summary(r):
     return out
 
 
+def small_batch_trace(iters=100):
+    """The library's concurrency sweep (ts_concurrency_sweep, seed 0) at 1, 2,
+    4 and 8 sequences, first with 4-token verify and then with one-token
+    decode: per point 20 untimed and `iters` timed attention calls back to
+    back, then the page-gather twin the same way.  Meant to run under a
+    kernel trace (rocprofv3 --kernel-trace), which gives every dispatch's
+    start and end; the returned points name what ran, in order, with what
+    each call launches (ts_decode_attn_plan) and the sweep's own times."""
+    import torch
+    from paper_2608_22788_amd import binding, synth
+    out = []
+    for vmax in (8, 0):
+        pts = binding.concurrency_sweep(batches=(1, 2, 4, 8), seeds=1, warmup=20, iters=iters,
+                                        verify_max_batch=vmax)
+        for pt in pts:
+            cfg = dict(synth.sweep_config(pt["batch"]))
+            cfg["q_len"] = pt["q_len"]
+            wl = synth.make_workload(f"sweep_b{pt['batch']}", seed=0, cfg=cfg)
+            maxp = wl.page_table.shape[1]
+            plan = binding.decode_attn_plan(binding.make_shape(wl.B, wl.Hq, wl.Hkv, wl.D, wl.Qmax, maxp,
+                                                               wl.max_ctx_len, wl.num_pages))
+            out.append(dict(batch=pt["batch"], q_len=pt["q_len"], warmup=20, iters=iters,
+                            call_us=round(pt["t_median_us"], 2), gather_us=round(pt["gather_median_us"], 2),
+                            kv_bytes=pt["kv_bytes"], plan=plan_summary(plan),
+                            merge_kernel=plan["merge_blocks"] > 0))
+            log(f"[bench] small-batch trace: b={pt['batch']} q_len={pt['q_len']} call {pt['t_median_us']:.2f} us")
+    torch.cuda.synchronize()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -576,6 +606,9 @@ def main():
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the read-only ceiling kernels timed beside each workload")
     ap.add_argument("--only", choices=list(WORKLOADS), help="time one workload only (profiling)")
+    ap.add_argument("--small-trace", action="store_true",
+                    help="run the concurrency sweep at 1-8 sequences (4-token verify, then one-token "
+                         "decode) for a kernel trace, and print what ran; --steps sets its timed calls")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="with --only: first copy BYTES with the library's plain copy kernel, "
                          "so hardware byte counters can be scaled against a known transfer")
@@ -589,6 +622,10 @@ def main():
     from paper_2608_22788_amd import binding
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+
+    if args.small_trace:
+        print(json.dumps({"small_batch_trace": small_batch_trace(args.steps)}), flush=True)
+        return
 
     if args.only:
         if args.calibrate_copy:
