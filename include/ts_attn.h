@@ -80,10 +80,11 @@ typedef enum ts_status {
  * or 128; num_q_heads a multiple of num_kv_heads with group size
  * G = num_q_heads / num_kv_heads in 1..16 and G * max_q_len <= 64;
  * max_q_len in 1..16; num_seqs in 1..4096; num_seqs * num_kv_heads <= 2^18.
- * max_ctx_len is an upper bound on ctx_lens, used only for validation; the
- * launch grid depends on the shape alone.  num_workers = 0 lets the library choose how many workers (one
- * wavefront, or a four-wavefront team for verify at head_dim 128) share the
- * KV stream; a positive value fixes it (the result does not depend on it
+ * max_ctx_len is an upper bound on ctx_lens, used for validation and to size
+ * the automatic worker count; the launch grid depends on the shape alone.
+ * num_workers = 0 lets the library choose how many workers (one wavefront,
+ * or a four-wavefront team for verify at head_dim 128) share the KV stream;
+ * a positive value fixes it (the result does not depend on it
  * beyond rounding; tests use it to vary the split points).  variant selects
  * the kernel:
  *   TS_VARIANT_AUTO  the matrix-core kernel in which one wavefront holds
